@@ -1,0 +1,144 @@
+/*
+ * qx.h -- C ABI of libqx: group-wise low-bit quantized weights, dequantized
+ * and multiplied by fp16 activations on an MI355X (gfx950) GPU.
+ *
+ * The method (QuantX, arXiv 2505.07531): a weight matrix is quantized
+ * group-wise to b bits with group size g along the reduction axis -- the
+ * paper's WbA16Gg notation, Table 1 -- either uniformly (equally spaced
+ * levels) or with a non-uniform per-group codebook (Section 2.2; Figure 2a
+ * shows one group mapped to its codebook). Decoding is memory-bound, so the
+ * packing and the dequantization kernels decide the runtime (Section 2.4).
+ * This library is that runtime side: it packs codes and tables into one blob
+ * and runs the fused dequantize-and-multiply kernels on it.
+ *
+ * Conventions shared by every call
+ *   - W is n x k with rows = output features (the nn.Linear orientation); k
+ *     is the reduction axis and groups are g consecutive elements of a row.
+ *   - fp16 means IEEE binary16, passed as its uint16_t bit pattern.
+ *   - Host pointers are read synchronously. Device pointers must be 16-byte
+ *     aligned and stay valid until the work queued on the stream has run.
+ *   - Device calls enqueue work on `stream` (NULL = the null stream) and
+ *     return without synchronizing. They allocate no memory, keep no global
+ *     mutable state, and may be captured into a HIP graph.
+ *   - The caller owns every buffer and the stream.
+ *   - Errors are negative status codes, listed below; QX_OK is 0. Argument
+ *     errors are detected before anything is enqueued. An error raised by the
+ *     GPU while the kernel runs surfaces at the caller's synchronization.
+ *
+ * Packed layout (version 1). The paper fixes no bit layout (its layout
+ * figure, Figure 3b, is absent), so this library defines one:
+ *   C = k / 128 chunks of 128 consecutive codes per row; G = k / g groups.
+ *   Codes region, n*k*b/8 bytes at offset 0: chunk c of row n is 16*b bytes,
+ *   split into b slices of 16 bytes; slice s (chunk bytes 16s..16s+15) is at
+ *   byte offset ((n*b + s)*C + c)*16. Chunk bit p is bit p%8 of chunk byte
+ *   p/8. Inside a chunk:
+ *     b = 4: code i in chunk bits 4i..4i+3.
+ *     b = 3: chunk byte j (0..47) = A field (bits 0-2) | B field (bits 3-5)
+ *            | spare field (bits 6-7);
+ *            code i < 48 is the A field of byte i; code 48+j is the B field
+ *            of byte j; code 96+m (m < 32) keeps bits 0-1 in the spare field
+ *            of byte m and bit 2 in bit 6 + m/16 of byte 32 + m%16.
+ *   Metadata region at offset n*k*b/8:
+ *     uniform : uint32 per (row, group) at (n*G + j)*4 = scale | zero << 16.
+ *     codebook: 2^b fp16 entries per (row, group) at (n*G + j)*2^(b+1).
+ */
+#ifndef QX_H_
+#define QX_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* HIP's stream handle (the same declaration as hip_runtime_api.h). */
+typedef struct ihipStream_t* hipStream_t;
+
+enum { QX_UNIFORM = 0, QX_CODEBOOK = 1 };    /* qx_desc.kind */
+enum { QX_OUT_F16 = 0, QX_OUT_CODES = 1 };   /* qx_dequant out_kind */
+
+enum {
+  QX_OK = 0,
+  QX_E_ARG = -1,          /* null or misaligned pointer, malformed descriptor or table */
+  QX_E_UNSUPPORTED = -2,  /* well-formed but not built (e.g. bits = 2, group = 256) */
+  QX_E_SIZE = -3,         /* output capacity too small */
+  QX_E_HIP = -4           /* the HIP runtime refused the launch */
+};
+
+/*
+ * Descriptor of one quantized matrix.
+ *   n     rows (output features), n >= 0
+ *   k     reduction length, a positive multiple of 128 (at most 1 << 20)
+ *   bits  code width b: 3 or 4
+ *   group g: 32, 64 or 128
+ *   kind  QX_UNIFORM or QX_CODEBOOK
+ *   flags must be 0
+ */
+typedef struct {
+  int32_t n, k, bits, group, kind;
+  uint32_t flags;
+} qx_desc;
+
+/*
+ * qx_pack_layout -- write the packed blob of one quantized matrix (host).
+ * Passage: group-wise b-bit codes with per-group metadata (Table 1's WbA16Gg
+ * notation; uniform levels versus a per-group codebook, Section 2.2 and
+ * Figure 2a).
+ *   codes     uint8 [n][k] row-major, each < 2^bits.
+ *   scales    fp16 [n][k/g] (uniform; NULL for codebook). Must be finite.
+ *   zeros     fp16 [n][k/g] (uniform; NULL for codebook). Each must be an
+ *             integer in [0, 2^bits - 1] (the levels are scale*(q - zero)).
+ *   codebook  fp16 [n][k/g][2^bits] (codebook; NULL for uniform). Any values.
+ *   packed    output, host memory of `cap` bytes; NULL = size query only.
+ *   packed_size  receives the blob size (n*k*b/8 plus the tables); required.
+ * All pointers are host pointers. Pure and synchronous; returns QX_E_ARG for
+ * a bad descriptor, a missing table, an out-of-range code or zero-point or a
+ * non-finite scale, and QX_E_SIZE when cap < *packed_size (nothing written).
+ */
+int qx_pack_layout(const qx_desc* d, const uint8_t* codes, const uint16_t* scales,
+                   const uint16_t* zeros, const uint16_t* codebook, void* packed, size_t cap,
+                   size_t* packed_size);
+
+/*
+ * qx_dequant -- expand a packed blob into fp16 weights or raw codes (device).
+ * Passage: the custom dequantization kernels of Section 2.4.
+ *   packed   device blob written by qx_pack_layout (copied to the GPU).
+ *   out_kind QX_OUT_F16: out = fp16 W' [n][k], uniform W' = fp16_RNE(s*(q-z))
+ *            (the exact product, rounded once), codebook W' = C[q].
+ *            QX_OUT_CODES: out = uint8 codes [n][k].
+ *   out      device buffer of n*k*2 (F16) or n*k (CODES) bytes.
+ * Results are bit-exact with the definitions above.
+ */
+int qx_dequant(const qx_desc* d, const void* packed, int out_kind, void* out, hipStream_t stream);
+
+/*
+ * qx_gemv -- y = W' x for one activation vector (device).
+ * Passage: decoding, the memory-bound case of Section 2.4, with fp16
+ * activations (the A16 of Table 1).
+ *   packed  device blob; x fp16 [k]; y fp16 [n] (written, RNE from an fp32
+ *           accumulator). y must not overlap x or packed.
+ * Products of fp16 values are exact, sums are fp32 in a fixed order, so the
+ * result is deterministic run to run. n = 0 is a no-op.
+ */
+int qx_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
+            hipStream_t stream);
+
+/*
+ * qx_gemm -- Y = X W'^T for m activation rows (device; prefill).
+ * Passage: as qx_gemv, batched over m rows.
+ *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte
+ *   alignment suffices for Y). fp16 matrix-core products, fp32 accumulate,
+ *   RNE to fp16. m = 0 or n = 0 is a no-op; m must be <= 65536.
+ */
+int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
+            hipStream_t stream);
+
+/* Static string for a status code ("unknown status" for values not listed). */
+const char* qx_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QX_H_ */

@@ -1,0 +1,189 @@
+"""Python binding of libqx (include/qx.h): group-wise 3/4-bit quantized weights,
+dequantized and multiplied by fp16 activations on an MI355X.
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels. PyTorch supplies device memory and streams. If the library is not
+built, ``load()`` builds it in-tree with hipcc; if it cannot be loaded, every
+call raises -- there is no fallback.
+
+Functions keep the C names:
+  qx_pack_layout(desc, codes, scales=None, zeros=None, codebook=None) -> uint8 numpy blob
+  qx_dequant(desc, packed, out_kind, out, stream=None)
+  qx_gemv(desc, packed, x, y, stream=None)
+  qx_gemm(desc, packed, m, X, Y, stream=None)
+  qx_status_str(status)
+Tensor arguments are torch CUDA tensors (HIP device memory); ``stream`` is a
+torch stream (default: the current stream).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+from . import _build
+
+QX_UNIFORM, QX_CODEBOOK = 0, 1
+QX_OUT_F16, QX_OUT_CODES = 0, 1
+QX_OK, QX_E_ARG, QX_E_UNSUPPORTED, QX_E_SIZE, QX_E_HIP = 0, -1, -2, -3, -4
+
+LIB_PATH = _build.LIB
+
+
+class QxDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("kind", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+    def __repr__(self):
+        return (f"QxDesc(n={self.n}, k={self.k}, bits={self.bits}, group={self.group}, "
+                f"kind={self.kind}, flags={self.flags})")
+
+
+def desc(n: int, k: int, bits: int, group: int, kind: int, flags: int = 0) -> QxDesc:
+    return QxDesc(n, k, bits, group, kind, flags)
+
+
+class QxError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {qx_status_str(status)} ({status})")
+
+
+_lib = None
+
+
+def build() -> str:
+    """Compile libqx.so for gfx950 in-tree (always recompiles)."""
+    global _lib
+    _lib = None
+    return _build.build()
+
+
+def load():
+    """The loaded libqx (ctypes.CDLL); builds it first if it is not there."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            _build.build()
+        L = ctypes.CDLL(LIB_PATH)
+        P, sz = ctypes.c_void_p, ctypes.c_size_t
+        D = ctypes.POINTER(QxDesc)
+        L.qx_pack_layout.argtypes = [D, P, P, P, P, P, sz, ctypes.POINTER(sz)]
+        L.qx_pack_layout.restype = ctypes.c_int
+        L.qx_dequant.argtypes = [D, P, ctypes.c_int, P, P]
+        L.qx_dequant.restype = ctypes.c_int
+        L.qx_gemv.argtypes = [D, P, P, P, P]
+        L.qx_gemv.restype = ctypes.c_int
+        L.qx_gemm.argtypes = [D, P, ctypes.c_int32, P, P, P]
+        L.qx_gemm.restype = ctypes.c_int
+        L.qx_status_str.argtypes = [ctypes.c_int]
+        L.qx_status_str.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def qx_status_str(status: int) -> str:
+    return load().qx_status_str(int(status)).decode()
+
+
+def _np_ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(st: int, where: str):
+    if st != QX_OK:
+        raise QxError(st, where)
+
+
+def qx_packed_size(d: QxDesc) -> int:
+    size = ctypes.c_size_t(0)
+    _check(load().qx_pack_layout(ctypes.byref(d), None, None, None, None, None, 0,
+                                 ctypes.byref(size)), "qx_pack_layout")
+    return size.value
+
+
+def qx_pack_layout(d: QxDesc, codes: np.ndarray, scales=None, zeros=None, codebook=None,
+                   out: Optional[np.ndarray] = None) -> np.ndarray:
+    """Packed blob (host uint8 array) of codes [n][k] and binary16 tables."""
+    def c(a, dt):
+        return None if a is None else np.ascontiguousarray(a, dtype=dt)
+    codes, scales, zeros, codebook = c(codes, np.uint8), c(scales, np.uint16), c(zeros, np.uint16), \
+        c(codebook, np.uint16)
+    total = qx_packed_size(d)
+    if out is None:
+        out = np.empty(total, np.uint8)
+    size = ctypes.c_size_t(0)
+    _check(load().qx_pack_layout(ctypes.byref(d), _np_ptr(codes), _np_ptr(scales), _np_ptr(zeros),
+                                 _np_ptr(codebook), _np_ptr(out), out.nbytes, ctypes.byref(size)),
+           "qx_pack_layout")
+    return out[:size.value]
+
+
+def _dev_ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensors required")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def qx_dequant(d: QxDesc, packed, out_kind: int, out, stream=None) -> None:
+    _check(load().qx_dequant(ctypes.byref(d), _dev_ptr(packed), out_kind, _dev_ptr(out),
+                             _stream(stream)), "qx_dequant")
+
+
+def qx_gemv(d: QxDesc, packed, x, y, stream=None) -> None:
+    _check(load().qx_gemv(ctypes.byref(d), _dev_ptr(packed), _dev_ptr(x), _dev_ptr(y),
+                          _stream(stream)), "qx_gemv")
+
+
+def qx_gemm(d: QxDesc, packed, m: int, X, Y, stream=None) -> None:
+    _check(load().qx_gemm(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(X), _dev_ptr(Y),
+                          _stream(stream)), "qx_gemm")
+
+
+# ------------------------------------------------------------- conveniences
+class PackedWeight:
+    """A packed matrix resident in device memory, with its descriptor."""
+
+    def __init__(self, d: QxDesc, blob: np.ndarray, device="cuda"):
+        import torch
+        self.desc = d
+        self.nbytes = int(blob.size)
+        self.data = torch.from_numpy(np.ascontiguousarray(blob)).to(device)
+
+    @classmethod
+    def from_quant(cls, q, device="cuda") -> "PackedWeight":
+        """From an object with n, k, bits, group, kind, codes, scales, zeros, codebook."""
+        d = desc(q.n, q.k, q.bits, q.group, q.kind)
+        return cls(d, qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook), device)
+
+    def dequant(self, out_kind: int = QX_OUT_F16, stream=None):
+        import torch
+        dt = torch.float16 if out_kind == QX_OUT_F16 else torch.uint8
+        out = torch.empty((self.desc.n, self.desc.k), dtype=dt, device=self.data.device)
+        qx_dequant(self.desc, self.data, out_kind, out, stream)
+        return out
+
+    def gemv(self, x, y=None, stream=None):
+        import torch
+        if y is None:
+            y = torch.empty(self.desc.n, dtype=torch.float16, device=x.device)
+        qx_gemv(self.desc, self.data, x, y, stream)
+        return y
+
+    def gemm(self, X, Y=None, stream=None):
+        import torch
+        m = X.shape[0]
+        if Y is None:
+            Y = torch.empty((m, self.desc.n), dtype=torch.float16, device=X.device)
+        qx_gemm(self.desc, self.data, m, X, Y, stream)
+        return Y

@@ -1,0 +1,146 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+entry point, packs byte-identically with the oracle, and returns the
+documented status codes. No kernel is launched here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import qx_inputs as qi
+from qx_inputs import configs
+import paper_2505_07531_amd as qx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "qx.h")) as f:
+        hdr = f.read()
+    declared = set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(qx_\w+)\s*\(", hdr, re.M))
+    assert {"qx_pack_layout", "qx_dequant", "qx_gemv", "qx_gemm", "qx_status_str"} <= declared
+    lib = ctypes.CDLL(qx.LIB_PATH if os.path.exists(qx.LIB_PATH) else qx.build())
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+
+
+def _random_quant(n, k, bits, group, kind, seed):
+    rng = np.random.default_rng(seed)
+    G = k // group
+    codes = rng.integers(0, 2**bits, (n, k), dtype=np.uint8)
+    if kind == 0:
+        s = np.float16(rng.uniform(1e-4, 1, (n, G))).view(np.uint16)
+        z = np.float16(rng.integers(0, 2**bits, (n, G))).view(np.uint16)
+        return codes, s, z, None
+    cb = np.float16(rng.standard_normal((n, G, 2**bits))).view(np.uint16)
+    return codes, None, None, cb
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("n,k", [(1, 128), (7, 384), (300, 256), (3, 11008)])
+def test_pack_layout_matches_oracle_bytes(bits, kind, group, n, k):
+    codes, s, z, cb = _random_quant(n, k, bits, group, kind, n + k + bits)
+    d = qx.desc(n, k, bits, group, kind)
+    blob = qx.qx_pack_layout(d, codes, s, z, cb)
+    ref = oracle.pack(codes, bits, group, kind, scales=s, zeros=z, codebook=cb)
+    assert blob.size == ref.size == oracle.packed_size(n, k, bits, group, kind)
+    assert np.array_equal(blob, ref)
+
+
+@pytest.mark.parametrize("make", [configs.c1, configs.c2, configs.c3])
+def test_pack_layout_full_config_matches_oracle(make):
+    spec, _ = make()
+    q = spec.quantized()
+    d = qx.desc(q.n, q.k, q.bits, q.group, q.kind)
+    blob = qx.qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook)
+    ref = oracle.pack(q.codes, q.bits, q.group, q.kind, q.scales, q.zeros, q.codebook)
+    assert blob.size == spec.packed_bytes
+    assert np.array_equal(blob, ref)
+
+
+def _st(fn):
+    try:
+        fn()
+    except qx.QxError as e:
+        return e.status
+    return qx.QX_OK
+
+
+def test_descriptor_errors():
+    codes = np.zeros((1, 128), np.uint8)
+    s = np.float16([[1.0]]).view(np.uint16)
+    z = np.float16([[0.0]]).view(np.uint16)
+    good = dict(n=1, k=128, bits=3, group=128, kind=0)
+    for change, want in [(dict(bits=2), qx.QX_E_UNSUPPORTED), (dict(bits=8), qx.QX_E_UNSUPPORTED),
+                         (dict(bits=0), qx.QX_E_ARG), (dict(bits=9), qx.QX_E_ARG),
+                         (dict(k=100), qx.QX_E_ARG), (dict(k=0), qx.QX_E_ARG),
+                         (dict(n=-1), qx.QX_E_ARG), (dict(group=0), qx.QX_E_ARG),
+                         (dict(group=48), qx.QX_E_ARG), (dict(group=256, k=256), qx.QX_E_UNSUPPORTED),
+                         (dict(group=16), qx.QX_E_UNSUPPORTED), (dict(kind=2), qx.QX_E_ARG)]:
+        p = {**good, **change}
+        d = qx.desc(p["n"], p["k"], p["bits"], p["group"], p["kind"])
+        assert _st(lambda: qx.qx_packed_size(d)) == want, change
+    d = qx.desc(1, 128, 3, 128, 0, flags=1)
+    assert _st(lambda: qx.qx_packed_size(d)) == qx.QX_E_ARG
+    d = qx.desc(1, 128, 3, 128, 0)
+    assert _st(lambda: qx.qx_pack_layout(d, codes, s, z)) == qx.QX_OK
+
+
+def test_pack_layout_value_errors_and_capacity():
+    d = qx.desc(2, 128, 3, 64, 0)
+    codes = np.zeros((2, 128), np.uint8)
+    s = np.float16(np.ones((2, 2))).view(np.uint16)
+    z = np.float16(np.zeros((2, 2))).view(np.uint16)
+    ok = lambda **kw: _st(lambda: qx.qx_pack_layout(d, **{**dict(codes=codes, scales=s, zeros=z), **kw}))
+    assert ok() == qx.QX_OK
+    assert ok(codes=np.full((2, 128), 8, np.uint8)) == qx.QX_E_ARG           # code >= 2^b
+    assert ok(zeros=np.float16(np.full((2, 2), 2.5)).view(np.uint16)) == qx.QX_E_ARG  # not integer
+    assert ok(zeros=np.float16(np.full((2, 2), 8.0)).view(np.uint16)) == qx.QX_E_ARG  # > 2^b - 1
+    assert ok(zeros=np.float16(np.full((2, 2), -1.0)).view(np.uint16)) == qx.QX_E_ARG
+    assert ok(scales=np.float16(np.full((2, 2), np.inf)).view(np.uint16)) == qx.QX_E_ARG
+    assert ok(scales=None) == qx.QX_E_ARG
+    assert qx.qx_packed_size(d) == 2 * 128 * 3 // 8 + 2 * 2 * 4
+    small = np.empty(qx.qx_packed_size(d) - 1, np.uint8)
+    assert _st(lambda: qx.qx_pack_layout(d, codes, s, z, out=small)) == qx.QX_E_SIZE
+    dc = qx.desc(2, 128, 3, 64, 1)
+    assert _st(lambda: qx.qx_pack_layout(dc, codes)) == qx.QX_E_ARG             # no codebook
+    cb = np.full((2, 2, 8), 0x7E00, np.uint16)                                 # NaN entries allowed
+    assert _st(lambda: qx.qx_pack_layout(dc, codes, codebook=cb)) == qx.QX_OK
+
+
+def test_empty_matrix():
+    d = qx.desc(0, 256, 4, 128, 0)
+    assert qx.qx_packed_size(d) == 0
+    assert qx.qx_pack_layout(d, np.zeros((0, 256), np.uint8), np.zeros((0, 2), np.uint16),
+                             np.zeros((0, 2), np.uint16)).size == 0
+
+
+def test_device_calls_reject_bad_arguments_before_launch():
+    lib = qx.load()
+    d = qx.desc(4, 128, 4, 128, 0)
+    P = ctypes.c_void_p
+    assert lib.qx_gemv(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemv(ctypes.byref(d), P(16), P(24), P(16), None) == qx.QX_E_ARG   # x misaligned
+    assert lib.qx_gemv(ctypes.byref(d), P(16), P(16), P(17), None) == qx.QX_E_ARG   # y odd address
+    assert lib.qx_dequant(ctypes.byref(d), P(16), 7, P(16), None) == qx.QX_E_ARG    # bad out_kind
+    assert lib.qx_dequant(ctypes.byref(d), P(8), 0, P(16), None) == qx.QX_E_ARG     # misaligned blob
+    assert lib.qx_gemm(ctypes.byref(d), P(16), -1, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemm(ctypes.byref(d), P(16), 70000, P(16), P(16), None) == qx.QX_E_ARG
+    bad = qx.desc(4, 128, 2, 128, 0)
+    assert lib.qx_gemv(ctypes.byref(bad), P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    assert lib.qx_gemv(None, P(16), P(16), P(16), None) == qx.QX_E_ARG
+    # empty work is a no-op that never reaches the runtime
+    z = qx.desc(0, 128, 4, 128, 0)
+    assert lib.qx_gemv(ctypes.byref(z), None, None, None, None) == qx.QX_OK
+    assert lib.qx_gemm(ctypes.byref(d), None, 0, None, None, None) == qx.QX_OK
+    assert lib.qx_dequant(ctypes.byref(z), None, 0, None, None) == qx.QX_OK
+
+
+def test_status_strings():
+    assert qx.qx_status_str(0) == "ok"
+    assert qx.qx_status_str(-3) == "output buffer too small"
+    assert qx.qx_status_str(99) == "unknown status"

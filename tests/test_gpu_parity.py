@@ -1,0 +1,171 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Dequantized codes and fp16 weights must be bit-exact. GEMV/GEMM outputs must
+satisfy max|y - y_ref| / max|y_ref| <= 2e-3 per output vector (fp32
+accumulation against fp64); one-hot activations must reproduce a column of
+W' bit-exactly, and repeated runs must be bitwise identical.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from qx_inputs import configs
+from helpers import TOL, activations, random_quant, realistic_quant, to_dev
+
+pytestmark = pytest.mark.gpu
+
+FORMATS = [(b, kind, g) for b in (3, 4) for kind in (0, 1) for g in (32, 64, 128)]
+SHAPES = [(1, 128), (3, 384), (37, 256), (5, 11008), (130, 4096)]
+
+
+def _fmt_id(f):
+    return f"b{f[0]}{'u' if f[1] == 0 else 'c'}g{f[2]}"
+
+
+def _ref_w16(q):
+    return oracle.dequant(q.codes, q.group, q.kind, q.scales, q.zeros, q.codebook)
+
+
+def _pack(qx, q):
+    return qx.PackedWeight.from_quant(q)
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_dequant_bit_exact(gpu, fmt, shape):
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = shape
+    print(f"dequant {fmt} {shape}", flush=True)
+    q = random_quant(n, k, bits, g, kind, seed=n * 7 + k + bits)
+    pw = _pack(qx, q)
+    codes = pw.dequant(qx.QX_OUT_CODES).cpu().numpy()
+    assert np.array_equal(codes, q.codes)
+    w16 = pw.dequant(qx.QX_OUT_F16).cpu().numpy()
+    assert np.array_equal(w16.view(np.uint16), _ref_w16(q).view(np.uint16))
+
+
+def test_dequant_tiny_scales_give_subnormal_halves(gpu):
+    qx = gpu
+    q = random_quant(4, 256, 3, 64, 0, seed=5, scale_range=(2.0**-24, 2.0**-16))
+    w16 = _pack(qx, q).dequant(qx.QX_OUT_F16).cpu().numpy()
+    ref = _ref_w16(q)
+    assert np.any((ref != 0) & (np.abs(ref.astype(np.float64)) < 2.0**-14))
+    assert np.array_equal(w16.view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("make", [configs.c1, configs.c2, configs.c3], ids=["c1", "c2", "c3"])
+def test_dequant_configs_bit_exact(gpu, make):
+    qx = gpu
+    spec, _ = make()
+    print(f"dequant {spec.name}", flush=True)
+    q = spec.quantized()
+    pw = _pack(qx, q)
+    assert np.array_equal(pw.dequant(qx.QX_OUT_CODES).cpu().numpy(), q.codes)
+    w16 = pw.dequant(qx.QX_OUT_F16).cpu().numpy()
+    assert np.array_equal(w16.view(np.uint16), _ref_w16(q).view(np.uint16))
+
+
+GEMV_SHAPES = SHAPES + [(33, 12288), (9, 16384), (260, 1024)]
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("shape", GEMV_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_gemv_matches_oracle(gpu, fmt, shape):
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = shape
+    print(f"gemv {fmt} {shape}", flush=True)
+    q = realistic_quant(n, k, bits, g, kind, seed=n + k)
+    x = activations(k, seed=k + bits)
+    pw = _pack(qx, q)
+    y = pw.gemv(to_dev(x)).cpu().numpy()
+    ref = oracle.gemv(_ref_w16(q), x)
+    err = oracle.normwise_rel_err(y, ref)
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+def test_gemv_one_hot_zero_and_determinism(gpu, fmt):
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = 70, 11008
+    q = random_quant(n, k, bits, g, kind, seed=bits * 10 + kind + g)
+    pw = _pack(qx, q)
+    w16 = _ref_w16(q)
+    for j in (0, 1, 47, 48, 95, 96, 127, 5000, k - 1):
+        x = np.zeros(k, np.float16)
+        x[j] = 1.0
+        y = pw.gemv(to_dev(x)).cpu().numpy()
+        # exact in value: a sum that starts at +0 cannot return -0, so -0 entries of W'
+        # (negative scale, q == z) come back as +0; every nonzero entry must match bit for bit
+        assert np.array_equal(y.astype(np.float64), w16[:, j].astype(np.float64)), j
+    y0 = pw.gemv(to_dev(np.zeros(k, np.float16))).cpu().numpy()
+    assert np.all(y0 == 0)
+    x = activations(k, seed=3)
+    xd = to_dev(x)
+    a = pw.gemv(xd).cpu().numpy()
+    b = pw.gemv(xd).cpu().numpy()
+    assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+@pytest.mark.parametrize("make", [configs.c1, configs.c2, configs.c3], ids=["c1", "c2", "c3"])
+def test_gemv_configs(gpu, make):
+    qx = gpu
+    spec, x = make()
+    print(f"gemv {spec.name}", flush=True)
+    q = spec.quantized()
+    pw = _pack(qx, q)
+    y = pw.gemv(to_dev(x)).cpu().numpy()
+    ref = oracle.gemv(_ref_w16(q), x)
+    err = oracle.normwise_rel_err(y, ref)
+    print(f"{spec.name} normwise rel err {err:.3e}")
+    assert err <= TOL, err
+
+
+GEMM_M = [1, 3, 16, 17, 33, 64, 65]
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("m", GEMM_M)
+def test_gemm_matches_oracle(gpu, fmt, m):
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = 100, 384
+    print(f"gemm {fmt} m={m}", flush=True)
+    q = realistic_quant(n, k, bits, g, kind, seed=m + bits)
+    X = activations(k, seed=m, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    ref = oracle.gemm(X, _ref_w16(q))
+    for r in range(m):
+        assert oracle.normwise_rel_err(Y[r], ref[r]) <= TOL, r
+
+
+@pytest.mark.parametrize("m", [16, 64, 512])
+@pytest.mark.parametrize("name", ["gate", "down"])
+def test_gemm_prefill_shapes(gpu, m, name):
+    qx = gpu
+    spec = configs.c5_matrix(name)
+    print(f"gemm c5 {name} m={m}", flush=True)
+    q = spec.quantized()
+    xin, xdn = configs.c5_activations(m)
+    X = xdn if name == "down" else xin
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    rows = range(m) if m <= 64 else range(0, m, 37)
+    w16 = _ref_w16(q)
+    for r in rows:
+        ref = oracle.gemv(w16, X[r])
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
+
+
+def test_gemm_rows_equal_gemv_within_tolerance(gpu):
+    qx = gpu
+    q = realistic_quant(257, 1024, 3, 64, 0, seed=11)
+    X = activations(1024, seed=12, m=9)
+    pw = _pack(qx, q)
+    Y = pw.gemm(to_dev(X)).cpu().numpy()
+    for r in range(9):
+        y = pw.gemv(to_dev(X[r])).cpu().numpy()
+        assert oracle.normwise_rel_err(Y[r], y.astype(np.float64)) <= 2 * TOL
