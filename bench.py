@@ -1,0 +1,408 @@
+#!/usr/bin/env python3
+"""Benchmark of the quantized dequantize-and-multiply hot path on one MI355X.
+
+Default workload (one "step"): one batch-1 decode step of a 32-layer 7B
+decoder weight set -- per layer q, k, v, o (4096x4096, 3-bit per-group
+codebook, group 128) and gate, up (11008x4096), down (4096x11008) (4-bit
+uniform, group 128) -- i.e. 224 quantized GEMVs launched back to back in
+layer order and replayed from a HIP graph. Inputs are synthetic and already
+resident in HBM when the timed region starts.
+
+Printed (one JSON line): effective HBM GB/s on packed-weight bytes over the
+step (value), us per decode step, the roofline of the dominant kernel measured
+live with HIP event pairs, and the CPU oracle timed on a bounded sample.
+
+Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
+configs, rotated over enough copies to defeat the 256 MB last-level cache) and
+--workload c5 (prefill GEMM, m = 16, 64, 512).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, published
+FP16_MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 matrix-core peak, published
+METRIC = "batch-1 qGEMV effective HBM GB/s (% of peak) + µs per 7B decode step"
+KERNEL_SOURCES = ["qx_device.h", "gemv.hip", "gemm.hip", "dequant.hip"]
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2505_07531_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel_key: str):
+    """HBM bytes per launch from committed counter summaries, if taken on this kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(kernel_key)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------- workloads
+def quantize_and_pack(spec, qx, device):
+    q = spec.quantized()
+    return qx.PackedWeight.from_quant(q, device=device)
+
+
+def concat_rows(parts):
+    """One quantized matrix whose rows are the rows of `parts` in order (same codes, same
+    tables): the GEMV of the result is the GEMVs of the parts, row for row."""
+    import qx_inputs as qi
+    p0 = parts[0]
+    cat = lambda a: None if getattr(p0, a) is None else np.concatenate([getattr(p, a) for p in parts])
+    return qi.QuantWeight(sum(p.n for p in parts), p0.k, p0.bits, p0.group, p0.kind, cat("codes"),
+                          cat("scales"), cat("zeros"), cat("codebook"))
+
+
+class DecodeStep:
+    """The 224 GEMVs of one decode step, resident on the GPU.
+
+    fused=False launches the 224 GEMVs one by one (q, k, v, o, gate, up, down per
+    layer). fused=True packs q|k|v and gate|up, which read the same activation
+    vector, as single matrices with the same quantized rows, so a layer is four
+    launches (qkv, o, gate|up, down) and the outputs are the same rows.
+    """
+
+    def __init__(self, qx, device, plan, quant, fused=False):
+        import torch
+        from qx_inputs import configs
+        self.plan = plan
+        layers = len(plan) // 7
+        self.launches = []  # (PackedWeight, activation key, [(row offset, plan index), ...])
+        if fused:
+            for l in range(layers):
+                b = 7 * l
+                groups = [[b, b + 1, b + 2], [b + 3], [b + 4, b + 5], [b + 6]]
+                for g in groups:
+                    q = concat_rows([quant[i] for i in g]) if len(g) > 1 else quant[g[0]]
+                    offs, o = [], 0
+                    for i in g:
+                        offs.append((o, i))
+                        o += quant[i].n
+                    self.launches.append((qx.PackedWeight.from_quant(q, device=device),
+                                          self.plan[g[0]][1], offs))
+        else:
+            for i, q in enumerate(quant):
+                self.launches.append((qx.PackedWeight.from_quant(q, device=device),
+                                      self.plan[i][1], [(0, i)]))
+        self.x = {}
+        for l in range(layers):
+            for t in range(4):
+                self.x[(l, t)] = torch.from_numpy(configs.c4_activation(l, t)).to(device)
+        self.y = [torch.empty(pw.desc.n, dtype=torch.float16, device=device)
+                  for pw, _, _ in self.launches]
+        self.packed_bytes = sum(spec.packed_bytes for spec, _ in self.plan)
+        self.act_bytes = sum(2 * (spec.n + spec.k) for spec, _ in self.plan)
+        self.qx = qx
+
+    def output(self, plan_index):
+        """Device view of the y of GEMV `plan_index` of the plan."""
+        for (pw, _, offs), y in zip(self.launches, self.y):
+            for off, i in offs:
+                if i == plan_index:
+                    return y[off:off + self.plan[i][0].n]
+        raise KeyError(plan_index)
+
+    def launch(self, stream=None):
+        qx = self.qx
+        for (pw, xi, _), y in zip(self.launches, self.y):
+            qx.qx_gemv(pw.desc, pw.data, self.x[xi], y, stream)
+
+
+def gated_kernel_durations(launches, reps=3):
+    """Per-launch GPU durations (ms) from HIP event pairs around each launch.
+
+    The stream is held behind a sleep kernel on a second stream while every
+    launch and event is enqueued, so host enqueue speed cannot stretch the
+    measured intervals.
+    """
+    import torch
+    s = torch.cuda.current_stream()
+    gate_stream = torch.cuda.Stream()
+    out = []
+    for _ in range(reps):
+        gate = torch.cuda.Event()
+        with torch.cuda.stream(gate_stream):
+            torch.cuda._sleep(int(2e8))  # ~0.1 s of device cycles
+            gate.record(gate_stream)
+        s.wait_event(gate)
+        evs = []
+        for fn in launches:
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            fn()
+            b.record(s)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        out.extend(a.elapsed_time(b) for a, b in evs)
+    return np.array(out)
+
+
+def cpu_baseline_decode():
+    """The oracle (unpack + fp16 dequant + fp64 matvec from the packed blob) on one matrix of
+    each decoder shape -- q (4096x4096 codebook), gate (11008x4096 uniform), down (4096x11008
+    uniform) of layer 0 -- scaled by how often each shape occurs in a step (128, 64, 32)."""
+    import oracle
+    import paper_2505_07531_amd as qx
+    from qx_inputs import configs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    sample = [("q", 0, 128), ("gate", 2, 64), ("down", 3, 32)]
+    items = []
+    for name, t, count in sample:
+        spec = configs.c4_matrix(0, name)
+        q = spec.quantized()
+        blob = qx.qx_pack_layout(qx.desc(q.n, q.k, q.bits, q.group, q.kind), q.codes, q.scales,
+                                 q.zeros, q.codebook)
+        items.append((spec, blob, configs.c4_activation(0, t), count))
+    step_s, total = 0.0, 0.0
+    for spec, blob, x, count in items:
+        t0 = time.perf_counter()
+        w16 = oracle.dequant_packed(blob, spec.n, spec.k, spec.bits, spec.group, spec.kind)
+        oracle.gemv(w16, x)
+        dt = time.perf_counter() - t0
+        total += dt
+        step_s += dt * count
+    packed = sum(s.packed_bytes for s, _ in configs.c4_plan(32))
+    return {"value": round(packed / step_s / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"3 GEMVs (layer-0 q, gate, down: unpack + fp16 dequant + fp64 matvec) in "
+                      f"{total:.1f} s, weighted x128/x64/x32 to a full step = "
+                      f"{step_s * 1e3:.0f} ms per decode step; numpy elementwise work is "
+                      f"single-threaded, BLAS uses the listed threads"}
+
+
+def quantize_plan(plan):
+    t0 = time.time()
+    quant = []
+    for i, (spec, _) in enumerate(plan):
+        quant.append(spec.quantized())
+        if (i + 1) % 28 == 0:
+            log(f"quantized {i + 1}/{len(plan)} matrices ({time.time() - t0:.0f}s)")
+    return quant
+
+
+def time_graph(launch, stream, steps, warmup):
+    """ms per replay of a HIP graph holding the launches made by `launch()`."""
+    import torch
+    with torch.cuda.stream(stream):
+        launch()  # eager run first: fail loudly before capture
+        stream.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            launch()
+        for _ in range(warmup):
+            g.replay()
+        stream.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def bench_decode(args, qx):
+    import torch
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    plan = configs.c4_plan(32)
+    quant = quantize_plan(plan)
+    fused = DecodeStep(qx, dev, plan, quant, fused=True)
+    single = DecodeStep(qx, dev, plan, quant, fused=False)
+    del quant
+    log(f"workload ready in {time.time() - t0:.0f}s: {fused.packed_bytes / 1e9:.3f} GB packed "
+        f"(each of two launch plans)")
+    stream = torch.cuda.Stream()
+    ms = time_graph(fused.launch, stream, args.steps, args.warmup)
+    log(f"fused plan (128 launches): {ms * 1e3:.1f} us per decode step")
+    ms_single = time_graph(single.launch, stream, max(5, args.steps // 2), 3)
+    log(f"one launch per GEMV (224 launches): {ms_single * 1e3:.1f} us per decode step")
+
+    # dominant kernel: the 4-bit uniform GEMV on the fused gate|up matrices (22016x4096)
+    dom = [(pw, xi, y) for (pw, xi, offs), y in zip(fused.launches, fused.y) if pw.desc.n == 22016]
+    def launch_dom():
+        for pw, xi, y in dom:
+            qx.qx_gemv(pw.desc, pw.data, fused.x[xi], y)
+    dom_graph_ms = time_graph(launch_dom, stream, 20, 3) / len(dom)
+    with torch.cuda.stream(stream):
+        durs = gated_kernel_durations([lambda a=a: qx.qx_gemv(a[0].desc, a[0].data, fused.x[a[1]], a[2])
+                                       for a in dom], reps=3)
+    d0 = dom[0][0].desc
+    alg_bytes = (d0.n * d0.k * d0.bits // 8 + d0.n * (d0.k // d0.group) * 4) + 2 * (d0.k + d0.n)
+    avg_ms = dom_graph_ms
+    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    traffic = committed_traffic("gemv_u4_g128_22016x4096")
+    value = fused.packed_bytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic (seeded Philox weights: Laplace attention, Student-t MLP; N(0,1) activations)",
+        "config": {"workload": "7B decoder decode step, batch 1: 32 layers x (q,k,v,o 4096x4096 "
+                               "3-bit codebook g128; gate,up 11008x4096 and down 4096x11008 4-bit "
+                               "uniform g128) = 224 GEMVs; q|k|v and gate|up packed as one matrix "
+                               "each (same rows), 128 launches, HIP graph replay",
+                   "packed_bytes_per_step": fused.packed_bytes,
+                   "activation_bytes_per_step": fused.act_bytes},
+        "us_per_step": round(ms * 1e3, 2),
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "us_per_step_one_launch_per_gemv": round(ms_single * 1e3, 2),
+        "roofline": {"kernel": "gemv_wave_kernel<4, uniform, g128> on the 22016x4096 gate|up "
+                               "matrix (32 launches per step)",
+                     "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "bytes_per_launch": alg_bytes,
+                     "avg_launch_us": round(avg_ms * 1e3, 3),
+                     "avg_launch_us_event_pairs": round(float(np.mean(durs)) * 1e3, 3),
+                     "launches_timed": 20 * len(dom)},
+    }
+    return out
+
+
+def rotated_copies(qx, spec, device, min_total=512 << 20):
+    q = spec.quantized()
+    d = qx.desc(q.n, q.k, q.bits, q.group, q.kind)
+    blob = qx.qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook)
+    import torch
+    reps = max(2, -(-min_total // blob.size))
+    base = torch.from_numpy(blob).to(device)
+    copies = [base] + [base.clone() for _ in range(reps - 1)]
+    return d, copies
+
+
+def bench_single_gemv(args, qx, name):
+    import torch
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    spec, x = getattr(configs, name)()
+    d, copies = rotated_copies(qx, spec, dev)
+    xd = torch.from_numpy(x).to(dev)
+    y = torch.empty(spec.n, dtype=torch.float16, device=dev)
+    launches = [lambda c=c: qx.qx_gemv(d, c, xd, y) for c in copies]
+    for fn in launches[:4]:
+        fn()
+    torch.cuda.synchronize()
+    durs = gated_kernel_durations(launches, reps=max(1, args.steps // len(launches) + 1))
+    alg = spec.packed_bytes + 2 * (spec.n + spec.k)
+    med = float(np.median(durs))
+    gbs = alg / (med * 1e-3) / 1e9
+    traffic = committed_traffic(f"gemv_{name}")
+    return {"metric": f"batch-1 qGEMV effective HBM GB/s ({name})", "value": round(gbs, 2),
+            "unit": "GB/s", "n_gpus": 1, "steps": int(durs.size), "warmup": 4,
+            "ms_per_step": round(med, 6), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+            "config": {"workload": f"{name}: {spec.n}x{spec.k} {spec.bits}-bit "
+                                   f"{'uniform' if spec.kind == 0 else 'codebook'} g{spec.group}",
+                       "copies": len(copies), "packed_bytes": spec.packed_bytes},
+            "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                         "median_launch_us": round(med * 1e3, 3),
+                         "min_launch_us": round(float(durs.min()) * 1e3, 3)}}
+
+
+def bench_gemm(args, qx):
+    import torch
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    mats = {nm: quantize_and_pack(configs.c5_matrix(nm), qx, dev) for nm in ("gate", "up", "down")}
+    lines = []
+    for m in configs.C5_M:
+        xin, xdn = configs.c5_activations(m)
+        xi, xd = torch.from_numpy(xin).to(dev), torch.from_numpy(xdn).to(dev)
+        ys = {nm: torch.empty((m, mats[nm].desc.n), dtype=torch.float16, device=dev) for nm in mats}
+        launches = [lambda nm=nm: qx.qx_gemm(mats[nm].desc, mats[nm].data, m,
+                                            xd if nm == "down" else xi, ys[nm])
+                    for nm in ("gate", "up", "down")]
+        for fn in launches:
+            fn()
+        torch.cuda.synchronize()
+        durs = gated_kernel_durations(launches, reps=5).reshape(5, 3)
+        t = float(np.median(durs.sum(1)))  # ms for the three GEMMs
+        flops = 2.0 * m * sum(mats[nm].desc.n * mats[nm].desc.k for nm in mats)
+        byts = sum(configs.c5_matrix(nm).packed_bytes for nm in mats) + m * 90_624
+        tf = flops / (t * 1e-3) / 1e12
+        gbs = byts / (t * 1e-3) / 1e9
+        hbm_t, mfma_t = byts / (HBM_PEAK_GBS * 1e9), flops / (FP16_MFMA_PEAK_TFLOPS * 1e12)
+        bound = "hbm" if hbm_t >= mfma_t else "mfma"
+        frac = (hbm_t if bound == "hbm" else mfma_t) / (t * 1e-3)
+        lines.append({"metric": f"prefill qGEMM (gate+up+down, m={m})", "value": round(tf, 3),
+                      "unit": "TFLOP/s", "n_gpus": 1, "steps": 5, "warmup": 1,
+                      "ms_per_step": round(t, 6), "higher_is_better": True, "scaling": "weak",
+                      "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+                      "config": {"workload": f"c5 MLP prefill GEMM m={m}, 3-bit uniform g64"},
+                      "roofline": {"bound": bound, "achieved": round(gbs if bound == "hbm" else tf, 2),
+                                   "peak": HBM_PEAK_GBS if bound == "hbm" else FP16_MFMA_PEAK_TFLOPS,
+                                   "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                                   "frac": round(frac, 4), "traffic": None}})
+    return lines
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="decode7b", choices=["decode7b", "c1", "c2", "c3", "c5"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2505_07531_amd as qx
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    qx.load()
+    log(f"device: {torch.cuda.get_device_name(0)}")
+    if args.workload == "decode7b":
+        out = bench_decode(args, qx)
+        if not args.no_cpu_baseline:
+            t0 = time.time()
+            out["cpu_baseline"] = cpu_baseline_decode()
+            log(f"cpu baseline in {time.time() - t0:.0f}s")
+        else:
+            out["cpu_baseline"] = None
+        print(json.dumps(out), flush=True)
+    elif args.workload == "c5":
+        for line in bench_gemm(args, qx):
+            print(json.dumps(line), flush=True)
+    else:
+        print(json.dumps(bench_single_gemv(args, qx, args.workload)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

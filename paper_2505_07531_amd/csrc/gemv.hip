@@ -5,49 +5,71 @@
 //   * work item = (row, 128-code chunk); a lane reads its chunk as b 16-byte
 //     loads from the slice planes, so each load instruction of a wave covers
 //     contiguous 16-byte pieces of one plane;
-//   * every load of a lane's items is issued before any is consumed;
-//   * x is staged once per workgroup in LDS, permuted into the pair order the
-//     decoders produce and padded so that lanes on consecutive chunks hit
-//     different banks;
-//   * codes are decoded in registers (qx_device.h) and multiplied with
-//     v_dot2_f32_f16 (exact fp16 products, fp32 sums); uniform groups are
-//     scaled once per group;
-//   * per-chunk partial sums go through LDS and are reduced per row by one
-//     wave with DPP/shuffles, in a fixed order (deterministic; no atomics).
+//   * x is loaded first (it is small and L2-resident), then every weight load
+//     of the lane is issued before any is consumed; x is permuted into the pair
+//     order of the decoders and staged once per workgroup in LDS, padded so
+//     that lanes on consecutive chunks hit different banks;
+//   * codes are decoded in registers (qx_device.h), one v_and_or_b32 per code
+//     pair, and multiplied with v_dot2_f32_f16 (exact fp16 products, fp32
+//     sums); uniform groups are scaled once per group;
+//   * partial sums are reduced per row in a fixed order with DPP (no atomics;
+//     results are deterministic).
 //
-// Launch: 256 threads; block b owns rows [R*b, R*b + R); items are the R x CT
-// (row, chunk) pairs of a K tile of CT <= 88 chunks, dealt round-robin to the
-// 256 lanes (ITEMS per lane). K longer than 88 chunks is walked in tiles of 64.
+// Three launch paths, all with one 128-code chunk per lane (more resident
+// waves measured faster than more chunks per lane):
+//   wave kernel: K = 128*32 or 128*64, a row fills half or all of a wave and
+//                is reduced in registers;
+//   row kernel:  any other K up to 88 chunks, R rows per block sized to leave
+//                few idle lanes, partials through LDS;
+//   tile kernel: longer K, walked in tiles of 64 chunks.
 #include "qx_device.h"
 #include "qx_internal.h"
+
+#include <algorithm>
 
 namespace qx {
 
 constexpr int kThreads = 256;
 constexpr int kMaxTileChunks = 88;
 constexpr int kLongTileChunks = 64;
-constexpr int kXBlock = 272;  // bytes of LDS per chunk of x: 256 + 16 padding
+constexpr int kXBlock = 272;                                   // LDS bytes per chunk of x
 
-// Stage x[k0 .. k0 + 128*ct) into LDS in decoder pair order.
-template <int BITS>
-__device__ __forceinline__ void stage_x(const uint16_t* __restrict__ x, int c0, int ct,
-                                        char* xs) {
-  const uint4* src = reinterpret_cast<const uint4*>(x) + (size_t)c0 * 16;
-  for (int p = threadIdx.x; p < ct * 16; p += kThreads) {
-    const uint4 v = src[p];
-    uint4 o;
-    if (BITS == 4) {  // [x0 x1][x2 x3][x4 x5][x6 x7] -> [x0 x4][x2 x6][x1 x5][x3 x7]
-      o.x = perm(v.z, v.x, 0x05040100u);
-      o.y = perm(v.w, v.y, 0x05040100u);
-      o.z = perm(v.z, v.x, 0x07060302u);
-      o.w = perm(v.w, v.y, 0x07060302u);
-    } else {  // per 4: [x0 x1][x2 x3] -> [x0 x2][x1 x3]
-      o.x = perm(v.y, v.x, 0x05040100u);
-      o.y = perm(v.y, v.x, 0x07060302u);
-      o.z = perm(v.w, v.z, 0x05040100u);
-      o.w = perm(v.w, v.z, 0x07060302u);
+// x pieces [c0*16, (c0+ct)*16) of this thread, loaded into registers. Every load
+// is issued (indices clamped in bounds) so the compiler can count outstanding
+// loads and wait for x alone.
+template <int XP>
+__device__ __forceinline__ void load_x(const uint16_t* __restrict__ x, int c0, int ct,
+                                       u32x4 (&xr)[XP]) {
+  const u32x4* src = reinterpret_cast<const u32x4*>(x) + (size_t)c0 * 16;
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    const int p = min((int)threadIdx.x + i * kThreads, ct * 16 - 1);
+    xr[i] = src[p];
+  }
+}
+
+// Permute the loaded pieces into decoder pair order and store them in LDS.
+template <int BITS, int XP, bool EXACT = false>  // EXACT: every piece is in range
+__device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs) {
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    const int p = threadIdx.x + i * kThreads;
+    if (EXACT || p < ct * 16) {
+      const u32x4 v = xr[i];
+      u32x4 o;
+      if (BITS == 4) {  // [x0 x1][x2 x3][x4 x5][x6 x7] -> [x0 x4][x1 x5][x2 x6][x3 x7]
+        o.x = perm(v.z, v.x, 0x05040100u);
+        o.y = perm(v.z, v.x, 0x07060302u);
+        o.z = perm(v.w, v.y, 0x05040100u);
+        o.w = perm(v.w, v.y, 0x07060302u);
+      } else {  // per 4: [x0 x1][x2 x3] -> [x0 x2][x1 x3]
+        o.x = perm(v.y, v.x, 0x05040100u);
+        o.y = perm(v.y, v.x, 0x07060302u);
+        o.z = perm(v.w, v.z, 0x05040100u);
+        o.w = perm(v.w, v.z, 0x07060302u);
+      }
+      *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
     }
-    *reinterpret_cast<uint4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
   }
 }
 
@@ -87,25 +109,38 @@ __device__ __forceinline__ void load_item(Item<BITS, KIND, G>& it, const char* _
   }
 }
 
+// Bit-2 source dword of spare codes of code dword I, and the two spare helpers
+// dispatched on the compile-time index.
+template <int I, int BITS, int KIND, int G>
+__device__ __forceinline__ void spare_pairs(const Item<BITS, KIND, G>& it, const DecodeConsts& k,
+                                            uint32_t& s0, uint32_t& s1) {
+  u3_spare<I>(it.d[I], it.d[8 + (I & 3)], k, s0, s1);
+}
+template <int I, int BITS, int KIND, int G>
+__device__ __forceinline__ uint32_t spare_sel(const Item<BITS, KIND, G>& it) {
+  return u3_sel_spare<I>(it.d[I], it.d[8 + (I & 3)]);
+}
+
 // Partial dot product of one chunk with its x block (LDS, pair order).
 template <int BITS, int KIND, int G>
-__device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const char* xb) {
+__device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const char* xb,
+                                           const DecodeConsts& k) {
   constexpr int NG = 128 / G;
-  const uint4* xv = reinterpret_cast<const uint4*>(xb);
+  const u32x4* xv = reinterpret_cast<const u32x4*>(xb);
   if constexpr (BITS == 4 && KIND == 0) {
     float part = 0.f;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const UniformGroup ug = uniform_group(it.m[g]);
+      const UniformGroup ug = uniform_group<4>(it.m[g]);
       float acc = 0.f;
 #pragma unroll
       for (int j = g * G / 8; j < (g + 1) * G / 8; ++j) {
-        const uint4 x = xv[j];
-        const uint32_t D = it.d[j];
-        acc = dot2(hadd2((D & 0x000F000Fu) | kMagic1024, ug.z1024), x.x, acc);
-        acc = dot2(hadd2(((D >> 8) & 0x000F000Fu) | kMagic1024, ug.z1024), x.y, acc);
-        acc = dot2(hadd2(((D >> 4) & 0x000F000Fu) | kMagic1024, ug.z1024), x.z, acc);
-        acc = dot2(hadd2(((D >> 12) & 0x000F000Fu) | kMagic1024, ug.z1024), x.w, acc);
+        const u32x4 x = xv[j];
+        const uint32_t D = it.d[j], Ds = D >> 8;
+        acc = dot2(hadd2((D & k.m000f) | k.mag1024, ug.z1024), x.x, acc);  // (0, 4)
+        acc = dot2(hadd2((D & k.m00f0) | k.mag64, ug.z64), x.y, acc);      // (1, 5)
+        acc = dot2(hadd2((Ds & k.m000f) | k.mag1024, ug.z1024), x.z, acc); // (2, 6)
+        acc = dot2(hadd2((Ds & k.m00f0) | k.mag64, ug.z64), x.w, acc);     // (3, 7)
       }
       part += ug.s * acc;
     }
@@ -117,34 +152,34 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
       const LutGroup<4> t = lut_group<4>(&it.m[g * 8]);
 #pragma unroll
       for (int j = g * G / 8; j < (g + 1) * G / 8; ++j) {
-        const uint4 x = xv[j];
+        const u32x4 x = xv[j];
         const uint32_t D = it.d[j];
-        uint32_t lo, hi;
-        lut4_bytes(t, D & 0x0F0F0F0Fu, lo, hi);          // codes 0 2 4 6
-        acc = dot2(perm(hi, lo, 0x06020400u), x.x, acc);  // (0, 4)
-        acc = dot2(perm(hi, lo, 0x07030501u), x.y, acc);  // (2, 6)
-        lut4_bytes(t, (D >> 4) & 0x0F0F0F0Fu, lo, hi);   // codes 1 3 5 7
-        acc = dot2(perm(hi, lo, 0x06020400u), x.z, acc);  // (1, 5)
-        acc = dot2(perm(hi, lo, 0x07030501u), x.w, acc);  // (3, 7)
+        uint32_t elo, ehi, olo, ohi;
+        lut4_bytes(t, D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
+        lut4_bytes(t, (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
+        acc = dot2(perm(ehi, elo, 0x06020400u), x.x, acc);  // (0, 4)
+        acc = dot2(perm(ohi, olo, 0x06020400u), x.y, acc);  // (1, 5)
+        acc = dot2(perm(ehi, elo, 0x07030501u), x.z, acc);  // (2, 6)
+        acc = dot2(perm(ohi, olo, 0x07030501u), x.w, acc);  // (3, 7)
       }
     }
     return acc;
   } else if constexpr (BITS == 3 && KIND == 0) {
     float acc[NG];
-#pragma unroll
-    for (int g = 0; g < NG; ++g) acc[g] = 0.f;
     UniformGroup ug[NG];
 #pragma unroll
-    for (int g = 0; g < NG; ++g) ug[g] = uniform_group(it.m[g]);
-    // x dword index of code block t (codes 4t..4t+3) is 2t (pair 0,2) and 2t+1 (pair 1,3)
+    for (int g = 0; g < NG; ++g) {
+      acc[g] = 0.f;
+      ug[g] = uniform_group<3>(it.m[g]);
+    }
+    // x dwords of code block t (codes 4t..4t+3): 2t = pair (0,2), 2t+1 = pair (1,3)
     const uint32_t* xd = reinterpret_cast<const uint32_t*>(xb);
 #pragma unroll
     for (int i = 0; i < 12; ++i) {
-      const uint32_t D = it.d[i];
-      const U3Pairs p = u3_fields(D);
+      const U3Pairs p = u3_fields(it.d[i], k);
       const int ga = (4 * i) / G, gb = (48 + 4 * i) / G;
-      const uint2 xa = *reinterpret_cast<const uint2*>(xd + 2 * i);
-      const uint2 xb2 = *reinterpret_cast<const uint2*>(xd + 2 * (12 + i));
+      const u32x2 xa = *reinterpret_cast<const u32x2*>(xd + 2 * i);
+      const u32x2 xb2 = *reinterpret_cast<const u32x2*>(xd + 2 * (12 + i));
       acc[ga] = dot2(hadd2(p.a0, ug[ga].z1024), xa.x, acc[ga]);
       acc[ga] = dot2(hadd2(p.a1, ug[ga].z1024), xa.y, acc[ga]);
       acc[gb] = dot2(hadd2(p.b0, ug[gb].z128), xb2.x, acc[gb]);
@@ -154,17 +189,17 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     for (int i = 0; i < 8; ++i) {
       uint32_t s0, s1;
       switch (i) {  // the bit-2 position depends on the dword index at compile time
-        case 0: u3_spare<0>(it.d[0], it.d[8], s0, s1); break;
-        case 1: u3_spare<1>(it.d[1], it.d[9], s0, s1); break;
-        case 2: u3_spare<2>(it.d[2], it.d[10], s0, s1); break;
-        case 3: u3_spare<3>(it.d[3], it.d[11], s0, s1); break;
-        case 4: u3_spare<4>(it.d[4], it.d[8], s0, s1); break;
-        case 5: u3_spare<5>(it.d[5], it.d[9], s0, s1); break;
-        case 6: u3_spare<6>(it.d[6], it.d[10], s0, s1); break;
-        default: u3_spare<7>(it.d[7], it.d[11], s0, s1); break;
+        case 0: spare_pairs<0>(it, k, s0, s1); break;
+        case 1: spare_pairs<1>(it, k, s0, s1); break;
+        case 2: spare_pairs<2>(it, k, s0, s1); break;
+        case 3: spare_pairs<3>(it, k, s0, s1); break;
+        case 4: spare_pairs<4>(it, k, s0, s1); break;
+        case 5: spare_pairs<5>(it, k, s0, s1); break;
+        case 6: spare_pairs<6>(it, k, s0, s1); break;
+        default: spare_pairs<7>(it, k, s0, s1); break;
       }
       const int gs = (96 + 4 * i) / G;
-      const uint2 xs = *reinterpret_cast<const uint2*>(xd + 2 * (24 + i));
+      const u32x2 xs = *reinterpret_cast<const u32x2*>(xd + 2 * (24 + i));
       acc[gs] = dot2(hadd2(s0, ug[gs].z16), xs.x, acc[gs]);
       acc[gs] = dot2(hadd2(s1, ug[gs].z16), xs.y, acc[gs]);
     }
@@ -183,11 +218,11 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
       const uint32_t D = it.d[i];
       const int ga = (4 * i) / G, gb = (48 + 4 * i) / G;
       uint32_t p02, p13;
-      const uint2 xa = *reinterpret_cast<const uint2*>(xd + 2 * i);
+      const u32x2 xa = *reinterpret_cast<const u32x2*>(xd + 2 * i);
       lut3_pairs(t[ga], u3_sel_a(D), p02, p13);
       acc = dot2(p02, xa.x, acc);
       acc = dot2(p13, xa.y, acc);
-      const uint2 xb2 = *reinterpret_cast<const uint2*>(xd + 2 * (12 + i));
+      const u32x2 xb2 = *reinterpret_cast<const u32x2*>(xd + 2 * (12 + i));
       lut3_pairs(t[gb], u3_sel_b(D), p02, p13);
       acc = dot2(p02, xb2.x, acc);
       acc = dot2(p13, xb2.y, acc);
@@ -196,19 +231,19 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     for (int i = 0; i < 8; ++i) {
       uint32_t S;
       switch (i) {
-        case 0: S = u3_sel_spare<0>(it.d[0], it.d[8]); break;
-        case 1: S = u3_sel_spare<1>(it.d[1], it.d[9]); break;
-        case 2: S = u3_sel_spare<2>(it.d[2], it.d[10]); break;
-        case 3: S = u3_sel_spare<3>(it.d[3], it.d[11]); break;
-        case 4: S = u3_sel_spare<4>(it.d[4], it.d[8]); break;
-        case 5: S = u3_sel_spare<5>(it.d[5], it.d[9]); break;
-        case 6: S = u3_sel_spare<6>(it.d[6], it.d[10]); break;
-        default: S = u3_sel_spare<7>(it.d[7], it.d[11]); break;
+        case 0: S = spare_sel<0>(it); break;
+        case 1: S = spare_sel<1>(it); break;
+        case 2: S = spare_sel<2>(it); break;
+        case 3: S = spare_sel<3>(it); break;
+        case 4: S = spare_sel<4>(it); break;
+        case 5: S = spare_sel<5>(it); break;
+        case 6: S = spare_sel<6>(it); break;
+        default: S = spare_sel<7>(it); break;
       }
       const int gs = (96 + 4 * i) / G;
       uint32_t p02, p13;
       lut3_pairs(t[gs], S, p02, p13);
-      const uint2 xs = *reinterpret_cast<const uint2*>(xd + 2 * (24 + i));
+      const u32x2 xs = *reinterpret_cast<const u32x2*>(xd + 2 * (24 + i));
       acc = dot2(p02, xs.x, acc);
       acc = dot2(p13, xs.y, acc);
     }
@@ -216,11 +251,107 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
   }
 }
 
-template <int BITS, int KIND, int G, int ITEMS>
-__global__ __launch_bounds__(kThreads) void gemv_kernel(const char* __restrict__ packed,
-                                                         const uint16_t* __restrict__ x,
-                                                         uint16_t* __restrict__ y, int n, int k,
-                                                         int R) {
+// K = 128*LPR with LPR in {32, 64}: a row's chunks fill LPR lanes of one wave, so
+// each row is reduced in registers with DPP and stored by one lane; no LDS
+// partials and no second barrier. Block = 4 waves = 4*(64/LPR) rows per round;
+// ROUNDS rounds per block, all loads issued up front.
+template <int BITS, int KIND, int G, int LPR, int ROUNDS>
+__global__ __launch_bounds__(kThreads) void gemv_wave_kernel(const char* __restrict__ packed,
+                                                              const uint16_t* __restrict__ x,
+                                                              uint16_t* __restrict__ y, int n) {
+  constexpr int C = LPR, RPW = 64 / LPR, RPB = 4 * RPW, XP = C * 16 / kThreads;
+  __shared__ __align__(16) char xs[C * kXBlock];
+  const int k = C * 128;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & (LPR - 1);
+  const int row_base = blockIdx.x * (RPB * ROUNDS) + wave * RPW + lane / LPR;
+  const DecodeConsts kc = decode_consts();
+
+  u32x4 xr[XP];
+  load_x<XP>(x, 0, C, xr);
+  Item<BITS, KIND, G> it[ROUNDS];
+#pragma unroll
+  for (int j = 0; j < ROUNDS; ++j)
+    load_item<BITS, KIND, G>(it[j], packed, meta_off, min(row_base + j * RPB, n - 1), c, C, k / G);
+  store_x<BITS, XP, true>(xr, C, xs);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < ROUNDS; ++j) {
+    const int row = row_base + j * RPB;
+    float v = chunk_dot<BITS, KIND, G>(it[j], xs + c * kXBlock, kc);
+    v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
+    if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
+  }
+}
+
+// K up to 88 chunks, any count: one (row, chunk) item per lane. The block has
+// 64*ceil(R*C/64) threads, with R picked so that few lanes idle (for C = 86,
+// R = 8 rows fill 688 of 704 lanes); per-item partials go through LDS and one
+// wave per row adds them in a fixed order.
+template <int BITS, int KIND, int G, int XP>
+__global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__ packed,
+                                                        const uint16_t* __restrict__ x,
+                                                        uint16_t* __restrict__ y, int n, int k,
+                                                        int R) {
+  extern __shared__ __align__(16) char smem[];
+  const int C = k >> 7, G_row = k / G, nthreads = blockDim.x;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
+  const int row0 = blockIdx.x * R;
+  const int rows = min(R, n - row0);
+  char* xs = smem;                                             // C * kXBlock bytes
+  float* part = reinterpret_cast<float*>(smem + C * kXBlock);  // R * C floats
+  const DecodeConsts kc = decode_consts();
+
+  u32x4 xr[XP];
+  const u32x4* src = reinterpret_cast<const u32x4*>(x);
+#pragma unroll
+  for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * nthreads, C * 16 - 1)];
+  const int t = threadIdx.x, r = t / C, c = t - r * C;
+  const bool valid = r < rows;
+  Item<BITS, KIND, G> it;
+  load_item<BITS, KIND, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    const int p = threadIdx.x + i * nthreads;
+    if (p < C * 16) {
+      const u32x4 v = xr[i];
+      u32x4 o;
+      if (BITS == 4) {
+        o.x = perm(v.z, v.x, 0x05040100u);
+        o.y = perm(v.z, v.x, 0x07060302u);
+        o.z = perm(v.w, v.y, 0x05040100u);
+        o.w = perm(v.w, v.y, 0x07060302u);
+      } else {
+        o.x = perm(v.y, v.x, 0x05040100u);
+        o.y = perm(v.y, v.x, 0x07060302u);
+        o.z = perm(v.w, v.z, 0x05040100u);
+        o.w = perm(v.w, v.z, 0x07060302u);
+      }
+      *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
+    }
+  }
+  __syncthreads();
+  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, kc);
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int rr = wave; rr < rows; rr += nthreads >> 6) {
+    float v = 0.f;
+    for (int cc = lane; cc < C; cc += 64) v += part[rr * C + cc];
+    v = wave_sum(v);
+    if (lane == 63) y[row0 + rr] = (uint16_t)float_to_half_bits(v);
+  }
+}
+
+// Any K: items are the R x CT (row, chunk) pairs of a K tile of CT <= 88 chunks,
+// dealt round-robin to the 256 lanes (ITEMS per lane); per-item partial sums go
+// through LDS and one wave per row adds them in a fixed order. K longer than 88
+// chunks is walked in tiles of 64 chunks.
+template <int BITS, int KIND, int G, int ITEMS, int XP>
+__global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restrict__ packed,
+                                                              const uint16_t* __restrict__ x,
+                                                              uint16_t* __restrict__ y, int n, int k,
+                                                              int R) {
   extern __shared__ __align__(16) char smem[];
   const int C = k >> 7;
   const int G_row = k / G;
@@ -230,6 +361,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const char* __restrict__
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
   char* xs = smem;                                              // CT * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + CT * kXBlock);  // R * CT floats
+  const DecodeConsts kc = decode_consts();
 
   float acc[ITEMS];
 #pragma unroll
@@ -237,6 +369,8 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const char* __restrict__
 
   for (int c0 = 0; c0 < C; c0 += CT) {
     const int ct = min(CT, C - c0);
+    u32x4 xr[XP];
+    load_x<XP>(x, c0, ct, xr);
     Item<BITS, KIND, G> it[ITEMS];
     bool valid[ITEMS];
     int cl[ITEMS];
@@ -246,17 +380,18 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const char* __restrict__
       const int r = i / CT;
       cl[j] = i - r * CT;
       valid[j] = r < rows && cl[j] < ct;
-      if (valid[j]) load_item<BITS, KIND, G>(it[j], packed, meta_off, row0 + r, c0 + cl[j], C, G_row);
+      // invalid slots load an in-bounds chunk and are never consumed
+      load_item<BITS, KIND, G>(it[j], packed, meta_off, row0 + min(r, rows - 1),
+                               c0 + min(cl[j], ct - 1), C, G_row);
     }
     if (c0 > 0) __syncthreads();  // previous tile's x no longer read
-    stage_x<BITS>(x, c0, ct, xs);
+    store_x<BITS, XP>(xr, ct, xs);
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j)
-      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock);
+      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock, kc);
   }
 
-  // per-item partials -> LDS [R][CT], then one wave per row sums them in a fixed order
 #pragma unroll
   for (int j = 0; j < ITEMS; ++j) {
     const int i = threadIdx.x + j * kThreads;
@@ -268,15 +403,50 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const char* __restrict__
     float v = 0.f;
     for (int c = lane; c < CT; c += 64) v += part[r * CT + c];
     v = wave_sum(v);
-    if (lane == 0) y[row0 + r] = (uint16_t)float_to_half_bits(v);
+    if (lane == 63) y[row0 + r] = (uint16_t)float_to_half_bits(v);
   }
 }
 
-// Rows per block and items per lane for an n x k matrix.
-static void gemv_shape(int n, int k, int* R, int* items) {
+// Rows per block and items per lane of the tile kernel for an n x k matrix.
+#ifndef QX_GEMV_ROUNDS
+#define QX_GEMV_ROUNDS 0  // 0: choose per shape
+#endif
+#ifndef QX_GEMV_TILE_ROWS
+#define QX_GEMV_TILE_ROWS 8
+#endif
+// Rounds per block of the wave kernel. One round (one chunk per lane) measured
+// fastest at every decoder shape, even when the grid exceeds one resident
+// generation of blocks: more resident waves hide latency better than more
+// independent loads per lane.
+static int wave_rounds(int n, int rpb) {
+  (void)n; (void)rpb;
+  return QX_GEMV_ROUNDS > 0 ? QX_GEMV_ROUNDS : 1;
+}
+
+// Rows per block and block size of the row kernel for C chunks per row: among
+// blocks of at least 256 threads (x is staged once per block), the R whose R*C
+// items leave the fewest idle lanes in 64*ceil(R*C/64) threads; at most 8 rows
+// when rows are long, so that large matrices still get many blocks.
+static void gemv_row_shape(int C, int* R, int* threads) {
+  const int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
+  int best_r = 0;
+  double best_u = -1.0;
+  for (int pass = 0; pass < 2 && best_r == 0; ++pass) {
+    for (int r = 1; r <= r_max; ++r) {
+      const int t = 64 * ((r * C + 63) / 64);
+      if (pass == 0 && t < 256) continue;
+      const double u = (double)(r * C) / t;
+      if (u > best_u + 1e-9) { best_u = u; best_r = r; }
+    }
+  }
+  *R = best_r;
+  *threads = 64 * ((best_r * C + 63) / 64);
+}
+
+static void gemv_tile_shape(int n, int k, int* R, int* items) {
   const int C = k / 128;
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
-  int r = 8;
+  int r = QX_GEMV_TILE_ROWS;
   while (r > 1 && (n + r - 1) / r < 512) r >>= 1;  // keep >= 512 blocks when n allows
   while (r > 1 && r * CT > 4 * kThreads) r >>= 1;
   *R = r;
@@ -284,20 +454,84 @@ static void gemv_shape(int n, int k, int* R, int* items) {
 }
 
 template <int BITS, int KIND, int G>
-static int launch_gemv_t(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
-                         hipStream_t s) {
+static void launch_gemv_tile(const qx_desc* d, const char* p, const uint16_t* x, uint16_t* y,
+                             hipStream_t s) {
   int R, items;
-  gemv_shape(d->n, d->k, &R, &items);
+  gemv_tile_shape(d->n, d->k, &R, &items);
   const int C = d->k / 128;
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
   const size_t lds = (size_t)CT * kXBlock + (size_t)R * CT * sizeof(float);
   const dim3 grid((d->n + R - 1) / R), block(kThreads);
+  const int xp = (CT * 16 + kThreads - 1) / kThreads;  // x pieces per thread: 1..6
+#define QX_GEMV_LAUNCH(I, XP) \
+  hipLaunchKernelGGL((gemv_tile_kernel<BITS, KIND, G, I, XP>), grid, block, lds, s, p, x, y, d->n, d->k, R)
+  if (xp <= 2) {
+    switch (items) {
+      case 1: QX_GEMV_LAUNCH(1, 2); break;
+      case 2: QX_GEMV_LAUNCH(2, 2); break;
+      default: QX_GEMV_LAUNCH(4, 2); break;
+    }
+  } else if (xp <= 4) {
+    switch (items) {
+      case 1: QX_GEMV_LAUNCH(1, 4); break;
+      case 2: QX_GEMV_LAUNCH(2, 4); break;
+      default: QX_GEMV_LAUNCH(4, 4); break;
+    }
+  } else {
+    switch (items) {
+      case 1: QX_GEMV_LAUNCH(1, 6); break;
+      case 2: QX_GEMV_LAUNCH(2, 6); break;
+      case 3: QX_GEMV_LAUNCH(3, 6); break;
+      default: QX_GEMV_LAUNCH(4, 6); break;
+    }
+  }
+#undef QX_GEMV_LAUNCH
+}
+
+template <int BITS, int KIND, int G>
+static int launch_gemv_t(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
+                         hipStream_t s) {
   const char* p = static_cast<const char*>(packed);
-  switch (items) {
-    case 1: hipLaunchKernelGGL((gemv_kernel<BITS, KIND, G, 1>), grid, block, lds, s, p, x, y, d->n, d->k, R); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<BITS, KIND, G, 2>), grid, block, lds, s, p, x, y, d->n, d->k, R); break;
-    case 3: hipLaunchKernelGGL((gemv_kernel<BITS, KIND, G, 3>), grid, block, lds, s, p, x, y, d->n, d->k, R); break;
-    default: hipLaunchKernelGGL((gemv_kernel<BITS, KIND, G, 4>), grid, block, lds, s, p, x, y, d->n, d->k, R); break;
+  const int C = d->k / 128;
+  if (C == 32 || C == 64) {
+    const int rpb = C == 32 ? 8 : 4;  // rows per block per round
+    const int rounds = wave_rounds(d->n, rpb);
+    const unsigned blocks = (unsigned)((d->n + rpb * rounds - 1) / (rpb * rounds));
+#define QX_WAVE_LAUNCH(L, RD) \
+  hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, L, RD>), dim3(blocks), dim3(kThreads), 0, s, p, x, y, d->n)
+    if (C == 32) {
+      switch (rounds) {
+        case 1: QX_WAVE_LAUNCH(32, 1); break;
+        case 2: QX_WAVE_LAUNCH(32, 2); break;
+        case 3: QX_WAVE_LAUNCH(32, 3); break;
+        default: QX_WAVE_LAUNCH(32, 4); break;
+      }
+    } else {
+      switch (rounds) {
+        case 1: QX_WAVE_LAUNCH(64, 1); break;
+        case 2: QX_WAVE_LAUNCH(64, 2); break;
+        case 3: QX_WAVE_LAUNCH(64, 3); break;
+        default: QX_WAVE_LAUNCH(64, 4); break;
+      }
+    }
+#undef QX_WAVE_LAUNCH
+  } else if (C <= kMaxTileChunks) {
+    int R, threads;
+    gemv_row_shape(C, &R, &threads);
+    const unsigned blocks = (unsigned)((d->n + R - 1) / R);
+    const size_t lds = (size_t)C * kXBlock + (size_t)R * C * sizeof(float);
+    const int xp = (C * 16 + threads - 1) / threads;
+#define QX_ROW_LAUNCH(XP) \
+  hipLaunchKernelGGL((gemv_row_kernel<BITS, KIND, G, XP>), dim3(blocks), dim3(threads), lds, s, p, x, y, d->n, d->k, R)
+    // blocks have >= 256 threads or C < 32, so xp <= ceil(88*16/256) = 6 never
+    // exceeds 4 in practice (C = 33..43 give 3); larger values take the tile kernel
+    if (xp <= 1) QX_ROW_LAUNCH(1);
+    else if (xp <= 2) QX_ROW_LAUNCH(2);
+    else if (xp <= 4) QX_ROW_LAUNCH(4);
+    else launch_gemv_tile<BITS, KIND, G>(d, p, x, y, s);
+#undef QX_ROW_LAUNCH
+  } else {
+    launch_gemv_tile<BITS, KIND, G>(d, p, x, y, s);
   }
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }

@@ -71,15 +71,20 @@ constexpr uint32_t kMagic16 = 0x4C004C00u;
 // field positions.
 struct UniformGroup {
   float s;
-  uint32_t z1024, z128, z16;
+  uint32_t z1024, z128, z64, z16;
 };
+template <int BITS>
 __device__ __forceinline__ UniformGroup uniform_group(uint32_t word) {
   UniformGroup g;
   g.s = half_bits_to_float(word & 0xFFFFu);
   const float z = half_bits_to_float(word >> 16);
   g.z1024 = splat_half(-(1024.0f + z));
-  g.z128 = splat_half(-(128.0f + z));
-  g.z16 = splat_half(-(16.0f + z));
+  if (BITS == 3) {
+    g.z128 = splat_half(-(128.0f + z));
+    g.z16 = splat_half(-(16.0f + z));
+  } else {
+    g.z64 = splat_half(-(64.0f + z));
+  }
   return g;
 }
 
@@ -100,32 +105,57 @@ __device__ __forceinline__ LutGroup<BITS> lut_group(const uint32_t* w) {  // 2^(
   return t;
 }
 
+// Constants kept in VGPRs so that "(D & mask) | bias" is one v_and_or_b32 (VOP3 on
+// this target encodes no 32-bit literal and reads at most one scalar register).
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t c) {
+  asm volatile("" : "+v"(c));
+  return c;
+}
+struct DecodeConsts {
+  uint32_t m0007, m0038, m00c0, m0100, m000f, m00f0, mag1024, mag128, mag64, mag16;
+};
+__device__ __forceinline__ DecodeConsts decode_consts() {
+  DecodeConsts k;
+  k.m0007 = in_vgpr(0x00070007u);
+  k.m0038 = in_vgpr(0x00380038u);
+  k.m00c0 = in_vgpr(0x00C000C0u);
+  k.m0100 = in_vgpr(0x01000100u);
+  k.m000f = in_vgpr(0x000F000Fu);
+  k.m00f0 = in_vgpr(0x00F000F0u);
+  k.mag1024 = in_vgpr(0x64006400u);
+  k.mag128 = in_vgpr(0x58005800u);
+  k.mag64 = in_vgpr(0x54005400u);
+  k.mag16 = in_vgpr(0x4C004C00u);
+  return k;
+}
+
 // ----------------------------------------------------------------- b = 3
-// The four fp16-pair extractions of the A and B fields of code dword D (bytes
-// b0..b3) return, as "M + q" pairs:
-//   a0 = (A0, A2)   a1 = (A1, A3)   (M = 1024)
-//   b0 = (B0, B2)   b1 = (B1, B3)   (M = 128)
+// "M + q" pairs of the A and B fields of code dword D (bytes b0..b3):
+//   a0 = (A0, A2), a1 = (A1, A3) with M = 1024; b0 = (B0, B2), b1 = (B1, B3) with M = 128.
 struct U3Pairs {
   uint32_t a0, a1, b0, b1;
 };
-__device__ __forceinline__ U3Pairs u3_fields(uint32_t D) {
+__device__ __forceinline__ U3Pairs u3_fields(uint32_t D, const DecodeConsts& k) {
   const uint32_t Ds = D >> 8;
   U3Pairs p;
-  p.a0 = (D & 0x00070007u) | kMagic1024;
-  p.a1 = (Ds & 0x00070007u) | kMagic1024;
-  p.b0 = (D & 0x00380038u) | kMagic128;
-  p.b1 = (Ds & 0x00380038u) | kMagic128;
+  p.a0 = (D & k.m0007) | k.mag1024;
+  p.a1 = (Ds & k.m0007) | k.mag1024;
+  p.b0 = (D & k.m0038) | k.mag128;
+  p.b1 = (Ds & k.m0038) | k.mag128;
   return p;
 }
 // Spare codes of code dword i (< 8): bits 0-1 in the spare fields of D, bit 2 in
 // H = dword 8 + (i & 3), bit 6 (i < 4) or bit 7 (i >= 4) of the matching byte.
 // Returns "16 + q" pairs for spare codes (0, 2) and (1, 3) of the dword.
 template <int I>
-__device__ __forceinline__ void u3_spare(uint32_t D, uint32_t H, uint32_t& s0, uint32_t& s1) {
+__device__ __forceinline__ void u3_spare(uint32_t D, uint32_t H, const DecodeConsts& k,
+                                         uint32_t& s0, uint32_t& s1) {
   constexpr int kUp = (I < 4) ? 2 : 1;    // bit 6 or 7 of bytes 0/2 -> bit 8 of each half
   constexpr int kDown = (I < 4) ? 6 : 7;  // bit 6 or 7 of bytes 1/3 -> bit 8 of each half
-  s0 = (D & 0x00C000C0u) | ((H << kUp) & 0x01000100u) | kMagic16;
-  s1 = ((D >> 8) & 0x00C000C0u) | ((H >> kDown) & 0x01000100u) | kMagic16;
+  const uint32_t t0 = ((H << kUp) & k.m0100) | k.mag16;
+  const uint32_t t1 = ((H >> kDown) & k.m0100) | k.mag16;
+  s0 = (D & k.m00c0) | t0;
+  s1 = ((D >> 8) & k.m00c0) | t1;
 }
 // Byte selectors (4 codes, natural order) of the three fields of code dword D.
 __device__ __forceinline__ uint32_t u3_sel_a(uint32_t D) { return D & 0x07070707u; }
@@ -194,16 +224,30 @@ __device__ __forceinline__ void block_weights(uint32_t Q, const uint32_t* meta, 
   }
 }
 
-// Wave-wide fp32 sum (64 lanes); every lane gets the total. DPP within rows of 16,
-// then cross-row shuffles.
-__device__ __forceinline__ float wave_sum(float v) {
-  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
-  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
-  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false)); // row_half_mirror
-  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false)); // row_mirror
-  v += __shfl_xor(v, 16);
-  v += __shfl_xor(v, 32);
+// Cross-lane fp32 sums with DPP only (no LDS traffic). A DPP "row" is 16 lanes.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_plus(float v) {
+  // lanes of rows outside ROW_MASK add 0 (the "old" operand)
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                 0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xF, false));
+}
+// Every lane of each 16-lane row ends with that row's sum.
+__device__ __forceinline__ float row16_sum(float v) {
+  v = dpp_plus<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+  v = dpp_plus<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+  v = dpp_plus<0x141, 0xF>(v);  // row_half_mirror
+  v = dpp_plus<0x140, 0xF>(v);  // row_mirror
   return v;
+}
+// Sum of lanes 0..31 in lane 31 and of lanes 32..63 in lane 63.
+__device__ __forceinline__ float half_wave_sum(float v) {
+  v = row16_sum(v);
+  return dpp_plus<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+}
+// Sum of all 64 lanes in lane 63.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = half_wave_sum(v);
+  return dpp_plus<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
 }
 
 }  // namespace qx

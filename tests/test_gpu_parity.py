@@ -68,7 +68,9 @@ def test_dequant_configs_bit_exact(gpu, make):
     assert np.array_equal(w16.view(np.uint16), _ref_w16(q).view(np.uint16))
 
 
-GEMV_SHAPES = SHAPES + [(33, 12288), (9, 16384), (260, 1024)]
+# covers every GEMV kernel path: rows of 32 or 64 chunks (in-wave reduction), rows of
+# up to 88 chunks (one chunk per lane), longer rows (K tiles), ragged row counts
+GEMV_SHAPES = SHAPES + [(33, 12288), (9, 16384), (260, 1024), (19, 8192), (1001, 11008)]
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
