@@ -1,0 +1,66 @@
+"""Full-size decode step (32 layers, 224 GEMVs) in the launch configuration the
+benchmark times: q|k|v and gate|up packed as single matrices, graph replay.
+
+The oracle computes sampled rows of every GEMV one by one (fp64 on the fp16
+dequantized rows); the normwise bound is taken over the sampled rows, which is
+stricter than over the whole vector. Launching the 224 GEMVs one by one must
+give bit-identical outputs (same rows, same codes, same kernels).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from qx_inputs import configs
+from helpers import TOL
+
+pytestmark = pytest.mark.gpu
+
+SAMPLED_ROWS = 48
+
+
+@pytest.fixture(scope="module")
+def decode_steps(gpu):
+    import torch
+    import bench
+    plan = configs.c4_plan(32)
+    print("quantizing the 224 decoder matrices", flush=True)
+    quant = bench.quantize_plan(plan)
+    dev = torch.device("cuda:0")
+    fused = bench.DecodeStep(gpu, dev, plan, quant, fused=True)
+    single = bench.DecodeStep(gpu, dev, plan, quant, fused=False)
+    stream = torch.cuda.Stream()
+    print("replaying both launch plans", flush=True)
+    bench.time_graph(fused.launch, stream, steps=2, warmup=1)
+    bench.time_graph(single.launch, stream, steps=2, warmup=1)
+    torch.cuda.synchronize()
+    yield plan, quant, fused, single
+    del fused, single
+    torch.cuda.empty_cache()
+
+
+def test_decode_step_sampled_rows_match_oracle(decode_steps):
+    plan, quant, fused, _ = decode_steps
+    rng = np.random.default_rng(0)
+    worst = 0.0
+    for i, (spec, (layer, t)) in enumerate(plan):
+        q = quant[i]
+        rows = np.sort(rng.choice(spec.n, SAMPLED_ROWS, replace=False))
+        rows[0], rows[-1] = 0, spec.n - 1  # always include the first and the last row
+        w16 = oracle.dequant(q.codes[rows], q.group, q.kind,
+                             None if q.scales is None else q.scales[rows],
+                             None if q.zeros is None else q.zeros[rows],
+                             None if q.codebook is None else q.codebook[rows])
+        ref = oracle.gemv(w16, configs.c4_activation(layer, t))
+        y = fused.output(i).cpu().numpy()[rows]
+        err = oracle.normwise_rel_err(y, ref)
+        worst = max(worst, err)
+        assert err <= TOL, (spec.name, err)
+    print(f"worst sampled normwise rel err over 224 GEMVs: {worst:.3e}")
+
+
+def test_fused_and_single_launch_plans_agree_bitwise(decode_steps):
+    plan, _, fused, single = decode_steps
+    for i in range(len(plan)):
+        a = fused.output(i).cpu().numpy().view(np.uint16)
+        b = single.output(i).cpu().numpy().view(np.uint16)
+        assert np.array_equal(a, b), plan[i][0].name
