@@ -1,156 +1,472 @@
 // Batched quantized GEMM (prefill): Y[m][n] = sum_k X[m][k] W'[n][k].
 //
-// The product is a dense contraction once W' is dequantized, so it runs on the
-// matrix cores: per 128-wide K step a block dequantizes a 64-row x 128 W' tile
-// into LDS (fp16, natural K order; uniform W' = fp16(s*(q-z)) by one packed
-// fp16 multiply of exact integers) next to the matching X tile, and each wave
-// multiplies its 16 weight rows with every 16-row slice of X using
-// v_mfma_f32_16x16x32_f16 (fp16 inputs, fp32 accumulators).
+// Once W' is dequantized the product is a dense contraction, so it runs on the
+// matrix cores (v_mfma_f32_16x16x32_f16: fp16 operands, fp32 accumulators).
+// The weights are the B operand and reach LDS only as packed codes: every lane
+// dequantizes, in registers, exactly the eight weights that its B fragment
+// holds, so the decode work of a weight is paid once per block of activation
+// rows and no LDS bandwidth is spent on fp16 W'. The activations are staged in
+// LDS once per block and chunk, in the order in which the decoders emit weight
+// pairs.
 //
-// Launch: 256 threads (4 waves); block (bx, by) owns weight rows
-// [64 bx, 64 bx + 64) and activation rows [BM by, BM by + BM), BM = 16*MT.
+// Fragments. A 128-code chunk of one weight row splits into 16 fragments of
+// 8 codes; fragment f = 4t + g feeds k-step t (32 of the 128 k) of the MFMA
+// from lane group g = lane / 16. The split is chosen so that, at a given
+// k-step, all four lane groups decode the same kind of field with the same
+// instructions (only the source dword differs, fetched by a per-lane address),
+// and so that every field of one k-step lies in one quantization group whose
+// index depends on t alone:
+//   b = 4: fragment f is code dword f (codes 8f..8f+7), pairs (0,4) (1,5) (2,6) (3,7);
+//   b = 3: f < 12 is code dword f: codes 4f..4f+3 from bits 0-2 of its bytes and
+//          48+4f..48+4f+3 from bits 3-5, pairs (0,2) (1,3) of each; f >= 12 holds
+//          the spare codes 96+8p..96+8p+7 (p = f - 12) of code dwords 2p, 2p+1.
+// Uniform weights are dequantized exactly, fp16(s*(q-z)), by one packed add of
+// exact integers and one packed multiply (the same arithmetic as qx_dequant);
+// codebook weights are table entries fetched with v_perm_b32.
+//
+// Tiling. A block has four waves: KS of them split the chunks of a row
+// (round r gives wave ks chunk r*KS + ks) and 4/KS take different weight rows.
+// A wave owns 16*NT weight rows and 16*MT activation rows. Codes reach the
+// waves through LDS: the codes and group tables of the block's rows for the next
+// super-round (S rounds, S*KS chunks) are loaded in contiguous runs while the
+// current one is multiplied and are written to LDS at its end; each lane then
+// reads the dwords of its fragments from there. Activations are loaded DX
+// rounds ahead into registers and written to one of two LDS buffers, in decoder
+// pair order. One barrier per round, two per super-round. The KS partial tiles
+// are added in a fixed order through LDS, so results are deterministic.
 #include "qx_device.h"
 #include "qx_internal.h"
 
 namespace qx {
 
 constexpr int kGemmThreads = 256;
-constexpr int kBN = 64;
-constexpr int kRowBytes = 272;  // LDS row stride: 128 fp16 + 16 bytes of padding
+constexpr int kXRowBytes = 272;  // one activation row of one chunk (fragment order) + 16 B pad
 
-// Natural-order 4-code selector of block t (codes 4t..4t+3) of a chunk.
-template <int BITS, int T>
-__device__ __forceinline__ uint32_t block_sel(const uint32_t (&d)[4 * BITS]) {
-  if constexpr (BITS == 4) {
-    constexpr int j = T / 2;
-    const uint32_t lo = d[j] & 0x0F0F0F0Fu, hi = (d[j] >> 4) & 0x0F0F0F0Fu;
-    return (T & 1) ? perm(hi, lo, 0x07030602u) : perm(hi, lo, 0x05010400u);
-  } else if constexpr (T < 12) {
-    return u3_sel_a(d[T]);
-  } else if constexpr (T < 24) {
-    return u3_sel_b(d[T - 12]);
-  } else {
-    return u3_sel_spare<T - 24>(d[T - 24], d[8 + ((T - 24) & 3)]);
-  }
-}
+// Codes and group tables of one (weight row, chunk) as one lane needs them.
+template <int BITS, int KIND, int G>
+struct LaneCodes {
+  static constexpr int kDw = BITS == 4 ? 4 : 7;
+  static constexpr int kMetaDw = KIND == QX_UNIFORM ? 128 / G : (128 / G) << (BITS - 1);
+  uint32_t d[kDw];  // b = 3: d[0..2] code dwords g, 4+g, 8+g; d[3..4] dwords 2g, 2g+1;
+                    //        d[5..6] dwords 8+2(g&1), 9+2(g&1) (bit 2 of the spare codes)
+  uint32_t m[kMetaDw];
+};
 
-// Decode codes [32U, 32U + 32) of a chunk into 16 fp16 pairs.
-template <int BITS, int KIND, int G, int U>
-__device__ __forceinline__ void decode_quarter(const uint32_t (&d)[4 * BITS], const uint32_t* meta,
-                                               uint32_t (&w)[16]) {
-  constexpr int kMetaDw = KIND == QX_UNIFORM ? 1 : (1 << BITS) / 2;
+// LDS image of the codes and group tables of a block's weight rows for SC
+// consecutive chunks (one super-round). Rows are padded so that the 16 rows read
+// by one instruction start in different banks.
+template <int BITS, int KIND, int G, int SC>
+struct CodeTile {
+  static constexpr int kRowBytes = BITS * SC * 16;
+  static constexpr int kRowStride = kRowBytes + (272 - kRowBytes % 256) % 256;  // = 16 mod 256
+  static constexpr int kMetaRow = KIND == QX_UNIFORM ? SC * (128 / G) * 4 : SC * (128 / G) * (2 << BITS);
+  static constexpr int kMetaStride = kMetaRow + (KIND == QX_UNIFORM ? 4 : 16);
+};
+
+template <int BITS, int KIND, int G, int SC>
+__device__ __forceinline__ void read_lane_codes(LaneCodes<BITS, KIND, G>& lc, const char* ct,
+                                                const char* mt, int rl, int cl, int g) {
+  using T = CodeTile<BITS, KIND, G, SC>;
+  const char* row = ct + rl * T::kRowStride + cl * 16;
 #pragma unroll
-  for (int v = 0; v < 8; ++v) {
-    uint32_t Q;
-    switch (v) {
-      case 0: Q = block_sel<BITS, 8 * U + 0>(d); break;
-      case 1: Q = block_sel<BITS, 8 * U + 1>(d); break;
-      case 2: Q = block_sel<BITS, 8 * U + 2>(d); break;
-      case 3: Q = block_sel<BITS, 8 * U + 3>(d); break;
-      case 4: Q = block_sel<BITS, 8 * U + 4>(d); break;
-      case 5: Q = block_sel<BITS, 8 * U + 5>(d); break;
-      case 6: Q = block_sel<BITS, 8 * U + 6>(d); break;
-      default: Q = block_sel<BITS, 8 * U + 7>(d); break;
+  for (int t = 0; t < (BITS == 4 ? 4 : 3); ++t)
+    lc.d[t] = *reinterpret_cast<const uint32_t*>(row + t * SC * 16 + 4 * g);
+  if constexpr (BITS == 3) {
+    const u32x2 lo = *reinterpret_cast<const u32x2*>(row + (g >> 1) * SC * 16 + 8 * (g & 1));
+    const u32x2 hi = *reinterpret_cast<const u32x2*>(row + 2 * SC * 16 + 8 * (g & 1));
+    lc.d[3] = lo.x; lc.d[4] = lo.y; lc.d[5] = hi.x; lc.d[6] = hi.y;
+  }
+  constexpr int kDw = LaneCodes<BITS, KIND, G>::kMetaDw;
+  const char* mp = mt + rl * T::kMetaStride + cl * kDw * 4;
+  if constexpr (kDw == 1) {
+    lc.m[0] = *reinterpret_cast<const uint32_t*>(mp);
+  } else if constexpr (kDw == 2) {
+    const u32x2 v = *reinterpret_cast<const u32x2*>(mp);
+    lc.m[0] = v.x; lc.m[1] = v.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < kDw / 4; ++i) {
+      const u32x4 v = reinterpret_cast<const u32x4*>(mp)[i];
+      lc.m[4 * i] = v.x; lc.m[4 * i + 1] = v.y; lc.m[4 * i + 2] = v.z; lc.m[4 * i + 3] = v.w;
     }
-    const int g = (4 * (8 * U + v)) / G;
-    block_weights<BITS, KIND>(Q, meta + g * kMetaDw, w[2 * v], w[2 * v + 1]);
   }
 }
 
-template <int BITS, int KIND, int G, int MT>
+// Dequantization constants of the uniform groups of one (row, chunk): the scale
+// pair (s, s) and -(M + z) pairs for the bias magic numbers M of each field.
+template <int BITS, int G>
+struct GroupConsts {
+  uint32_t sp[128 / G], z1024[128 / G], zb[128 / G], z16[128 / G];  // zb: M = 128 (b=3), 64 (b=4)
+};
+template <int BITS, int G>
+__device__ __forceinline__ GroupConsts<BITS, G> group_consts(const uint32_t* m) {
+  GroupConsts<BITS, G> gc;
+#pragma unroll
+  for (int i = 0; i < 128 / G; ++i) {
+    const uint32_t w = m[i];
+    // z is an integer-valued fp16 in [0, 2^b - 1]; -(M + z) is exact in fp16 and its bits
+    // are those of -M plus z fraction steps
+    const uint32_t z = (uint32_t)(unsigned short)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+    gc.sp[i] = perm(w, w, 0x01000100u);
+    gc.z1024[i] = (0xE400u + z) * 0x00010001u;
+    gc.zb[i] = BITS == 3 ? (0xD800u + 8u * z) * 0x00010001u : (0xD400u + 16u * z) * 0x00010001u;
+    gc.z16[i] = (0xCC00u + 64u * z) * 0x00010001u;
+  }
+  return gc;
+}
+
+__device__ __forceinline__ uint32_t deq(uint32_t mq, uint32_t zc, uint32_t sp) {
+  return hmul2(hadd2(mq, zc), sp);  // fp16(s * (q - z)), q - z exact
+}
+
+__device__ __forceinline__ h8_t frag(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return __builtin_bit_cast(h8_t, u32x4{a, b, c, d});
+}
+
+// B fragment of k-step T for this lane (weights in register pair order).
+template <int BITS, int KIND, int G, int T>
+__device__ __forceinline__ h8_t decode_frag(const LaneCodes<BITS, KIND, G>& lc,
+                                            const GroupConsts<BITS, G>& gc,
+                                            const LutGroup<BITS> (&lut)[128 / G],
+                                            const DecodeConsts& k, uint32_t up, uint32_t dn,
+                                            uint32_t ssh) {
+  if constexpr (BITS == 4) {
+    constexpr int gr = (32 * T) / G;
+    const uint32_t D = lc.d[T], Ds = D >> 8;
+    if constexpr (KIND == QX_UNIFORM) {
+      return frag(deq((D & k.m000f) | k.mag1024, gc.z1024[gr], gc.sp[gr]),   // (0, 4)
+                  deq((D & k.m00f0) | k.mag64, gc.zb[gr], gc.sp[gr]),       // (1, 5)
+                  deq((Ds & k.m000f) | k.mag1024, gc.z1024[gr], gc.sp[gr]),  // (2, 6)
+                  deq((Ds & k.m00f0) | k.mag64, gc.zb[gr], gc.sp[gr]));     // (3, 7)
+    } else {
+      uint32_t elo, ehi, olo, ohi;
+      lut4_bytes(lut[gr], D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
+      lut4_bytes(lut[gr], (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
+      return frag(perm(ehi, elo, 0x06020400u), perm(ohi, olo, 0x06020400u),
+                  perm(ehi, elo, 0x07030501u), perm(ohi, olo, 0x07030501u));
+    }
+  } else if constexpr (T < 3) {
+    constexpr int ga = (16 * T) / G, gb = (48 + 16 * T) / G;
+    const uint32_t D = lc.d[T];
+    if constexpr (KIND == QX_UNIFORM) {
+      const U3Pairs p = u3_fields(D, k);
+      return frag(deq(p.a0, gc.z1024[ga], gc.sp[ga]), deq(p.a1, gc.z1024[ga], gc.sp[ga]),
+                  deq(p.b0, gc.zb[gb], gc.sp[gb]), deq(p.b1, gc.zb[gb], gc.sp[gb]));
+    } else {
+      uint32_t a02, a13, b02, b13;
+      lut3_pairs(lut[ga], u3_sel_a(D), a02, a13);
+      lut3_pairs(lut[gb], u3_sel_b(D), b02, b13);
+      return frag(a02, a13, b02, b13);
+    }
+  } else {
+    constexpr int gs = 96 / G;
+    uint32_t w[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t L = lc.d[3 + h], H = lc.d[5 + h];
+      if constexpr (KIND == QX_UNIFORM) {
+        // bit 6 (spare dwords 0-3) or 7 (4-7) of bytes 0/2 and 1/3 of H -> bit 8 of each half
+        const uint32_t t0 = ((H << up) & k.m0100) | k.mag16;
+        const uint32_t t1 = ((H >> dn) & k.m0100) | k.mag16;
+        w[2 * h] = deq((L & k.m00c0) | t0, gc.z16[gs], gc.sp[gs]);
+        w[2 * h + 1] = deq(((L >> 8) & k.m00c0) | t1, gc.z16[gs], gc.sp[gs]);
+      } else {
+        const uint32_t S = ((L >> 6) & 0x03030303u) | ((H >> ssh) & 0x04040404u);
+        lut3_pairs(lut[gs], S, w[2 * h], w[2 * h + 1]);
+      }
+    }
+    return frag(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Activation piece for fragment f of one row of one chunk: 16 bytes in the pair
+// order of decode_frag. lo/hi are the two 8-byte halves read from X.
+template <int BITS>
+__device__ __forceinline__ void x_piece_offsets(int f, int& o1, int& o2) {  // in elements
+  if (BITS == 4) {
+    o1 = 8 * f; o2 = o1 + 4;
+  } else {
+    o1 = f < 12 ? 4 * f : 96 + 8 * (f - 12);
+    o2 = f < 12 ? 48 + 4 * f : o1 + 4;
+  }
+}
+template <int BITS>
+__device__ __forceinline__ u32x4 x_piece(u32x2 lo, u32x2 hi) {
+  u32x4 o;
+  if (BITS == 4) {  // [x0 x1][x2 x3] [x4 x5][x6 x7] -> [x0 x4][x1 x5][x2 x6][x3 x7]
+    o.x = perm(hi.x, lo.x, 0x05040100u);
+    o.y = perm(hi.x, lo.x, 0x07060302u);
+    o.z = perm(hi.y, lo.y, 0x05040100u);
+    o.w = perm(hi.y, lo.y, 0x07060302u);
+  } else {  // per four: [x0 x1][x2 x3] -> [x0 x2][x1 x3]
+    o.x = perm(lo.y, lo.x, 0x05040100u);
+    o.y = perm(lo.y, lo.x, 0x07060302u);
+    o.z = perm(hi.y, hi.x, 0x05040100u);
+    o.w = perm(hi.y, hi.x, 0x07060302u);
+  }
+  return o;
+}
+
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX>
 __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restrict__ packed,
                                                              const uint16_t* __restrict__ X,
                                                              uint16_t* __restrict__ Y, int n,
-                                                             int k, int m) {
-  constexpr int BM = 16 * MT;
-  constexpr int kMetaDw = KIND == QX_UNIFORM ? 128 / G : (128 / G) * (1 << BITS) / 2;
-  __shared__ __align__(16) char xs[BM * kRowBytes];
-  __shared__ __align__(16) char ws[kBN * kRowBytes];
-  const int C = k >> 7, G_row = k / G;
+                                                             int k, int m, int nx, int my) {
+  constexpr int NG = 4 / KS;  // wave groups on different weight rows
+  constexpr int BM = 16 * MT, BN = 16 * NT * NG, SC = S * KS;
+  using CT = CodeTile<BITS, KIND, G, SC>;
+  constexpr int kXPieces = KS * BM * 16 / kGemmThreads;  // activation pieces per thread and round
+  constexpr int kXBuf = KS * BM * kXRowBytes;
+  constexpr int kCTotal = BN * BITS * SC;                                 // 16-byte code pieces
+  constexpr int kCPieces = (kCTotal + kGemmThreads - 1) / kGemmThreads;  // per thread
+  constexpr int kMetaUnit = KIND == QX_UNIFORM ? 4 : 16;   // bytes per table load
+  constexpr int kMPieces = (BN * CT::kMetaRow / kMetaUnit + kGemmThreads - 1) / kGemmThreads;
+  static_assert(KS * BM * 16 % kGemmThreads == 0, "activation pieces must divide evenly");
+  static_assert(S % DX == 0, "activation register sets must divide the super-round");
+  static_assert((KS - 1) * NG * MT * NT * 1024 <= 2 * kXBuf, "reduction must fit the LDS buffers");
+  __shared__ __align__(16) char xs[2 * kXBuf];
+  __shared__ __align__(16) char cts[BN * CT::kRowStride];
+  __shared__ __align__(16) char mts[BN * CT::kMetaStride];
+
+  // Block -> (weight tile bn, activation tile bm). With several activation tiles,
+  // the tiles of one weight tile go to one XCD (workgroups are dealt to the 8 XCDs
+  // round-robin), so its codes are fetched from HBM once and re-read from that L2.
+  int bn, bm;
+  if (my == 1) {
+    bn = blockIdx.x; bm = 0;
+  } else {
+    const int q = blockIdx.x >> 3;
+    bm = q % my;
+    bn = (q / my) * 8 + (blockIdx.x & 7);
+  }
+  if (bn >= nx) return;  // padding blocks of the XCD mapping: whole block, before any barrier
+  const int n0 = bn * BN, m0 = bm * BM;
+  const int C = k >> 7, G_row = k / G, R = (C + KS - 1) / KS, NSR = (R + S - 1) / S;
   const size_t meta_off = (size_t)n * k * BITS / 8;
-  const int n0 = blockIdx.x * kBN, m0 = blockIdx.y * BM;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wrow = n0 + lane;  // weight row this lane decodes
-  const bool wvalid = wrow < n;
+  const int ks = wave % KS, ng = wave / KS;
+  const int g = lane >> 4, li = lane & 15;
+  const DecodeConsts kc = decode_consts();
+  const uint32_t up = g < 2 ? 2u : 1u, dn = g < 2 ? 6u : 7u, ssh = g < 2 ? 4u : 5u;
 
-  f4_t acc[MT];
+  // Codes of super-round j (chunks [j*SC, j*SC + SC)) of the block's rows: contiguous
+  // runs of SC*16 bytes per (row, slice) and of the group tables per row, loaded
+  // into registers at the start of super-round j - 1 (rows and chunks clamped in
+  // bounds; the clamped copies are never multiplied) and written to LDS at its end.
+  auto load_codes = [&](int j, u32x4 (&cr)[kCPieces], u32x4 (&mr)[kMPieces]) {
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < kCPieces; ++i) {
+      const int p = min((int)threadIdx.x + i * kGemmThreads, kCTotal - 1);
+      const int cl = p % SC, sl = (p / SC) % BITS, rl = p / (SC * BITS);
+      const int row = min(n0 + rl, n - 1), c = min(j * SC + cl, C - 1);
+      cr[i] = *reinterpret_cast<const u32x4*>(packed + (((size_t)row * BITS + sl) * C + c) * 16);
+    }
+    constexpr int kUnits = CT::kMetaRow / kMetaUnit;  // per row
+#pragma unroll
+    for (int i = 0; i < kMPieces; ++i) {
+      const int p = min((int)threadIdx.x + i * kGemmThreads, BN * kUnits - 1);
+      const int ul = p % kUnits, rl = p / kUnits;
+      const int row = min(n0 + rl, n - 1);
+      // group index of this unit, clamped to the row's last group
+      const int gi = min(j * SC * (128 / G) + ul * kMetaUnit / (KIND == QX_UNIFORM ? 4 : 2 << BITS),
+                         G_row - 1);
+      const char* src = packed + meta_off + ((size_t)row * G_row + gi) * (KIND == QX_UNIFORM ? 4 : 2 << BITS);
+      if constexpr (KIND == QX_UNIFORM)
+        mr[i] = u32x4{*reinterpret_cast<const uint32_t*>(src), 0u, 0u, 0u};
+      else
+        mr[i] = *reinterpret_cast<const u32x4*>(src + (ul * 16) % (2 << BITS));
+    }
+  };
+  auto store_codes = [&](const u32x4 (&cr)[kCPieces], const u32x4 (&mr)[kMPieces]) {
+#pragma unroll
+    for (int i = 0; i < kCPieces; ++i) {
+      const int p = threadIdx.x + i * kGemmThreads;
+      const int cl = p % SC, sl = (p / SC) % BITS, rl = p / (SC * BITS);
+      if (kCTotal % kGemmThreads == 0 || p < kCTotal)
+        *reinterpret_cast<u32x4*>(cts + rl * CT::kRowStride + sl * SC * 16 + cl * 16) = cr[i];
+    }
+    constexpr int kUnits = CT::kMetaRow / kMetaUnit;
+#pragma unroll
+    for (int i = 0; i < kMPieces; ++i) {
+      const int p = threadIdx.x + i * kGemmThreads;
+      if (p < BN * kUnits) {
+        const int ul = p % kUnits, rl = p / kUnits;
+        char* dst = mts + rl * CT::kMetaStride + ul * kMetaUnit;
+        if constexpr (KIND == QX_UNIFORM)
+          *reinterpret_cast<uint32_t*>(dst) = mr[i].x;
+        else
+          *reinterpret_cast<u32x4*>(dst) = mr[i];
+      }
+    }
+  };
+  // activation pieces of round r into registers (rows and chunks clamped in bounds;
+  // rows past m are never stored, chunks past C are never multiplied)
+  auto load_x = [&](int r, u32x2 (&lo)[kXPieces], u32x2 (&hi)[kXPieces]) {
+#pragma unroll
+    for (int i = 0; i < kXPieces; ++i) {
+      const int p = threadIdx.x + i * kGemmThreads;
+      const int f = p & 15, ml = (p >> 4) % BM, kq = p / (16 * BM);
+      const int c = min(r * KS + kq, C - 1), row = min(m0 + ml, m - 1);
+      int o1, o2;
+      x_piece_offsets<BITS>(f, o1, o2);
+      const uint16_t* src = X + (size_t)row * k + (size_t)c * 128;
+      lo[i] = *reinterpret_cast<const u32x2*>(src + o1);
+      hi[i] = *reinterpret_cast<const u32x2*>(src + o2);
+    }
+  };
+  auto store_x = [&](int buf, const u32x2 (&lo)[kXPieces], const u32x2 (&hi)[kXPieces]) {
+#pragma unroll
+    for (int i = 0; i < kXPieces; ++i) {
+      const int p = threadIdx.x + i * kGemmThreads;
+      const int f = p & 15, ml = (p >> 4) % BM, kq = p / (16 * BM);
+      *reinterpret_cast<u32x4*>(xs + buf * kXBuf + (kq * BM + ml) * kXRowBytes + 16 * f) =
+          x_piece<BITS>(lo[i], hi[i]);
+    }
+  };
 
-  for (int c = 0; c < C; ++c) {
-    // X tile [BM][128]
-    for (int p = threadIdx.x; p < BM * 16; p += kGemmThreads) {
-      const int r = p >> 4, t = p & 15;
-      u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (m0 + r < m)
-        v = *reinterpret_cast<const u32x4*>(X + (size_t)(m0 + r) * k + (size_t)c * 128 + 8 * t);
-      *reinterpret_cast<u32x4*>(xs + r * kRowBytes + 16 * t) = v;
-    }
-    // W' tile: lane -> weight row, wave -> quarter of the chunk
-    if (wvalid) {
-      const u32x4* code = reinterpret_cast<const u32x4*>(packed) + ((size_t)wrow * BITS * C + c);
-      uint32_t d[4 * BITS];
+  f4_t acc[MT][NT];
 #pragma unroll
-      for (int s = 0; s < BITS; ++s) {
-        const u32x4 v = code[(size_t)s * C];
-        d[4 * s] = v.x; d[4 * s + 1] = v.y; d[4 * s + 2] = v.z; d[4 * s + 3] = v.w;
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 cr[kCPieces], mr[kMPieces];
+  load_codes(0, cr, mr);
+  store_codes(cr, mr);
+  // Activations: round r + DX is loaded into register set r % DX during round r, and
+  // round r + 1 (loaded DX - 1 rounds earlier) is written to LDS buffer (r + 1) & 1
+  // at its end, so every load has DX rounds to arrive.
+  u32x2 xlo[DX][kXPieces], xhi[DX][kXPieces];
+  load_x(0, xlo[0], xhi[0]);
+  store_x(0, xlo[0], xhi[0]);
+#pragma unroll
+  for (int i = 1; i < DX; ++i) load_x(i, xlo[i], xhi[i]);
+  __syncthreads();
+
+  // Every load is issued unconditionally (indices clamped in bounds) so that the
+  // compiler waits for exactly the loads a step consumes; rounds past the last
+  // chunk multiply nothing.
+  for (int j = 0; j < NSR; ++j) {
+    load_codes(j + 1, cr, mr);
+#pragma unroll
+    for (int u = 0; u < S; ++u) {
+      const int r = j * S + u;
+      load_x(r + DX, xlo[u % DX], xhi[u % DX]);
+      if (r * KS + ks < C) {
+        const char* xb = xs + (r & 1) * kXBuf + ks * BM * kXRowBytes;
+        LaneCodes<BITS, KIND, G> cur[NT];
+        GroupConsts<BITS, G> gc[NT];
+        LutGroup<BITS> lut[NT][128 / G];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          read_lane_codes<BITS, KIND, G, SC>(cur[nt], cts, mts, 16 * (ng * NT + nt) + li, u * KS + ks, g);
+          if constexpr (KIND == QX_UNIFORM) {
+            gc[nt] = group_consts<BITS, G>(cur[nt].m);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 128 / G; ++i) lut[nt][i] = lut_group<BITS>(&cur[nt].m[i << (BITS - 1)]);
+          }
+        }
+#define QX_GEMM_KSTEP(T)                                                                      \
+  {                                                                                           \
+    h8_t a[MT];                                                                               \
+    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const h8_t*>( \
+        xb + (16 * mt + li) * kXRowBytes + 64 * (T) + 16 * g);                                \
+    _Pragma("unroll") for (int nt = 0; nt < NT; ++nt) {                                       \
+      const h8_t b = decode_frag<BITS, KIND, G, T>(cur[nt], gc[nt], lut[nt], kc, up, dn, ssh); \
+      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) acc[mt][nt] =                         \
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(a[mt], b, acc[mt][nt], 0, 0, 0);             \
+    }                                                                                         \
+  }
+        QX_GEMM_KSTEP(0)
+        QX_GEMM_KSTEP(1)
+        QX_GEMM_KSTEP(2)
+        QX_GEMM_KSTEP(3)
+#undef QX_GEMM_KSTEP
       }
-      const size_t gidx = (size_t)wrow * G_row + (size_t)c * (128 / G);
-      const uint32_t* mp = reinterpret_cast<const uint32_t*>(
-          packed + meta_off + gidx * (KIND == QX_UNIFORM ? 4 : 2 * (1 << BITS)));
-      uint32_t meta[kMetaDw];
-#pragma unroll
-      for (int i = 0; i < kMetaDw; ++i) meta[i] = mp[i];
-      uint32_t w[16];
-      switch (wave) {
-        case 0: decode_quarter<BITS, KIND, G, 0>(d, meta, w); break;
-        case 1: decode_quarter<BITS, KIND, G, 1>(d, meta, w); break;
-        case 2: decode_quarter<BITS, KIND, G, 2>(d, meta, w); break;
-        default: decode_quarter<BITS, KIND, G, 3>(d, meta, w); break;
-      }
-      u32x4* dst = reinterpret_cast<u32x4*>(ws + lane * kRowBytes + 64 * wave);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i] = u32x4{w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
+      store_x((r + 1) & 1, xlo[(u + 1) % DX], xhi[(u + 1) % DX]);
+      __syncthreads();
     }
-    __syncthreads();
-    // MFMA: wave -> weight rows [16 wave, 16 wave + 16)
-    const int li = lane & 15, lq = lane >> 4;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const h8_t b = *reinterpret_cast<const h8_t*>(ws + (16 * wave + li) * kRowBytes + 64 * kk + 16 * lq);
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        const h8_t a = *reinterpret_cast<const h8_t*>(xs + (16 * t + li) * kRowBytes + 64 * kk + 16 * lq);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[t], 0, 0, 0);
-      }
-    }
+    store_codes(cr, mr);  // every wave is past the super-round's last read of the tile
     __syncthreads();
   }
-  // D[i][j]: lane holds rows 4*(lane/16) + r, column lane % 16
-  const int col = n0 + 16 * wave + (lane & 15);
-  if (col < n) {
+
+  // KS partial tiles -> one, in ks order, through LDS (every wave passed the last barrier)
+  if constexpr (KS > 1) {
+    float* red = reinterpret_cast<float*>(xs);
+    if (ks > 0) {
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = m0 + 16 * t + 4 * (lane >> 4) + r;
-        if (row < m) Y[(size_t)row * n + col] = (uint16_t)float_to_half_bits(acc[t][r]);
-      }
+        for (int nt = 0; nt < NT; ++nt)
+          *reinterpret_cast<f4_t*>(red + ((((ks - 1) * NG + ng) * MT + mt) * NT + nt) * 256 + 4 * lane) =
+              acc[mt][nt];
+    }
+    __syncthreads();
+    if (ks > 0) return;
+#pragma unroll
+    for (int q = 1; q < KS; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          acc[mt][nt] += *reinterpret_cast<const f4_t*>(
+              red + ((((q - 1) * NG + ng) * MT + mt) * NT + nt) * 256 + 4 * lane);
+  }
+
+  // D[i][j] of a 16x16 tile: lane holds rows 4*(lane/16) + r, column lane % 16
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int col = n0 + 16 * (ng * NT + nt) + li;
+    if (col < n) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + 16 * mt + 4 * g + r;
+          if (row < m) Y[(size_t)row * n + col] = (uint16_t)float_to_half_bits(acc[mt][nt][r]);
+        }
     }
   }
 }
 
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX>
+static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y,
+                            hipStream_t s) {
+  constexpr int BN = 16 * NT * (4 / KS), BM = 16 * MT;
+  const int nx = (d->n + BN - 1) / BN, my = (m + BM - 1) / BM;
+  const unsigned blocks = my == 1 ? (unsigned)nx : (unsigned)((nx + 7) / 8) * 8u * (unsigned)my;
+  hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, MT, NT, KS, S, DX>), dim3(blocks), dim3(kGemmThreads),
+                     0, s, p, X, Y, d->n, d->k, m, nx, my);
+}
+
+// Tile shape per activation row count. Small m is bound by streaming the codes:
+// one 16-row activation tile, 16 weight rows per block and the chunks of a row
+// split over the four waves, so that the grid has enough blocks. Larger m gets
+// larger activation tiles so that each decoded weight feeds more MFMAs; with
+// m > 64 a wave owns 64 activation x 32 weight rows.
+#ifndef QX_GEMM_CFG
+#define QX_GEMM_CFG 0  // 0: by m; 1, 2, 4 force one shape
+#endif
 template <int BITS, int KIND, int G>
 static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint16_t* X,
                          uint16_t* Y, hipStream_t s) {
   const char* p = static_cast<const char*>(packed);
-  const unsigned nb = (unsigned)((d->n + kBN - 1) / kBN);
-  if (m <= 16) {
-    hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, 1>), dim3(nb, (m + 15) / 16), dim3(kGemmThreads), 0, s, p, X, Y, d->n, d->k, m);
-  } else if (m <= 32) {
-    hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, 2>), dim3(nb, (m + 31) / 32), dim3(kGemmThreads), 0, s, p, X, Y, d->n, d->k, m);
-  } else {
-    hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, 4>), dim3(nb, (m + 63) / 64), dim3(kGemmThreads), 0, s, p, X, Y, d->n, d->k, m);
+  constexpr bool kUni = KIND == QX_UNIFORM;
+  const int cfg = QX_GEMM_CFG > 0 ? QX_GEMM_CFG : m <= 16 ? 1 : m <= 64 ? 2 : 4;
+  switch (cfg) {
+    case 1:
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 4, 4>(d, p, m, X, Y, s);
+      else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1>(d, p, m, X, Y, s);
+      break;
+    case 2:
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 4, 2>(d, p, m, X, Y, s);
+      else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
+      break;
+    default:
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2>(d, p, m, X, Y, s);
+      else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
+      break;
   }
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }

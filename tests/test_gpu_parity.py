@@ -162,6 +162,26 @@ def test_gemm_prefill_shapes(gpu, m, name):
         assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
 
 
+# activation tiles mapped to XCDs with padding blocks, single-chunk rows, chunk counts
+# that leave K-split waves idle in the last round
+GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40)]
+
+
+@pytest.mark.parametrize("fmt", [(3, 0, 64), (4, 0, 128), (3, 1, 32), (4, 1, 32)], ids=_fmt_id)
+@pytest.mark.parametrize("shape", GEMM_EDGES, ids=lambda s: f"{s[0]}x{s[1]}m{s[2]}")
+def test_gemm_tile_edges(gpu, fmt, shape):
+    qx = gpu
+    bits, kind, g = fmt
+    n, k, m = shape
+    print(f"gemm {fmt} {shape}", flush=True)
+    q = realistic_quant(n, k, bits, g, kind, seed=n + k + m)
+    X = activations(k, seed=m + 1, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    ref = oracle.gemm(X, _ref_w16(q))
+    for r in range(m):
+        assert oracle.normwise_rel_err(Y[r], ref[r]) <= TOL, r
+
+
 def test_gemm_rows_equal_gemv_within_tolerance(gpu):
     qx = gpu
     q = realistic_quant(257, 1024, 3, 64, 0, seed=11)
