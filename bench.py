@@ -10,11 +10,14 @@ resident in HBM when the timed region starts.
 
 Printed (one JSON line): effective HBM GB/s on packed-weight bytes over the
 step (value), us per decode step, the roofline of the dominant kernel measured
-live with HIP event pairs, and the CPU oracle timed on a bounded sample.
+live (HIP events around a graph of its launches, on the stream they run on),
+and the CPU oracle timed on a bounded sample.
 
 Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
-configs, rotated over enough copies to defeat the 256 MB last-level cache) and
---workload c5 (prefill GEMM, m = 16, 64, 512).
+configs, rotated over enough copies to defeat the 256 MB last-level cache),
+--workload c5 (prefill GEMM, m = 16, 64, 512), --workload floor (plain read of
+the same byte counts and empty grids: the floor of a one-launch GEMV) and
+--workload counters (the run that the FETCH_SIZE / WRITE_SIZE passes profile).
 """
 from __future__ import annotations
 
@@ -396,13 +399,51 @@ def bench_kernel_counters(args, qx):
             "copy_bytes_each_way": int(a.numel())}
 
 
+def bench_floor(args, qx):
+    """The floor of a one-launch GEMV: a plain coalesced read of the same number of
+    bytes (16 B per thread, cold: rotated over copies >= 512 MB, graph-timed), and an
+    empty grid of the decode kernels' block counts."""
+    import torch
+    from paper_2505_07531_amd import probe
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    sizes = {"q|k|v": 3 * configs.c4_matrix(0, "q").packed_bytes,
+             "o": configs.c4_matrix(0, "o").packed_bytes,
+             "gate|up": 2 * configs.c4_matrix(0, "gate").packed_bytes,
+             "down": configs.c4_matrix(0, "down").packed_bytes}
+    for name in ("c1", "c2", "c3"):
+        sizes[name] = getattr(configs, name)()[0].packed_bytes
+    stream = torch.cuda.Stream()
+    reads = []
+    for name, nbytes in sizes.items():
+        reps = max(2, -(-(512 << 20) // nbytes))
+        bufs = [torch.ones(nbytes, dtype=torch.uint8, device=dev) for _ in range(reps)]
+        def launch_all():
+            for b in bufs:
+                probe.qxp_read(b, sink)
+        us = time_graph(launch_all, stream, 5, 2) / reps * 1e3
+        reads.append({"matrix": name, "bytes": nbytes, "us": round(us, 3),
+                      "gbs": round(nbytes / (us * 1e-6) / 1e9, 1)})
+        log(f"read {name}: {nbytes} B in {us:.3f} us")
+        del bufs
+    empty = {}
+    for blocks in (1, 512, 1536, 2752):
+        def launch_empty():
+            for _ in range(100):
+                probe.qxp_empty(blocks, sink)
+        empty[str(blocks)] = round(time_graph(launch_empty, stream, 5, 2) / 100 * 1e3, 3)
+    return {"workload": "floor", "read": reads, "empty_grid_us_by_blocks": empty,
+            "note": "per launch, graph of back-to-back launches; 256 threads per block"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "c1", "c2", "c3", "c5", "counters"])
+                    choices=["decode7b", "c1", "c2", "c3", "c5", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -427,6 +468,8 @@ def main():
         print(json.dumps(out), flush=True)
     elif args.workload == "counters":
         print(json.dumps(bench_kernel_counters(args, qx)), flush=True)
+    elif args.workload == "floor":
+        print(json.dumps(bench_floor(args, qx)), flush=True)
     elif args.workload == "c5":
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)

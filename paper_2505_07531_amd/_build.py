@@ -1,4 +1,5 @@
-"""Build libqx.so (HIP kernels for gfx950 + the C-ABI front end) in-tree with hipcc."""
+"""Build libqx.so (HIP kernels for gfx950 + the C-ABI front end) and the measurement
+library libqxprobe.so in-tree with hipcc."""
 from __future__ import annotations
 
 import os
@@ -10,9 +11,11 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libqx.so")
+PROBE_LIB = os.path.join(PKG, "libqxprobe.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["qx_api.cpp", "dequant.hip", "gemv.hip", "gemm.hip"]
+PROBE_SOURCES = ["bw_probe.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc" if os.path.exists("/opt/rocm/bin/hipcc") else "hipcc")
 
@@ -32,18 +35,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build() -> str:
-    """Compile every source for gfx950 and link libqx.so next to this file."""
-    os.makedirs(OBJDIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(4, os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + f".tmp{os.getpid()}"
+def _link(objs, lib: str) -> str:
+    tmp = lib + f".tmp{os.getpid()}"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build() -> str:
+    """Compile every source for gfx950 and link libqx.so and libqxprobe.so next to
+    this file; returns the path of libqx.so."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=min(5, os.cpu_count() or 1)) as ex:
+        objs = list(ex.map(_compile, SOURCES + PROBE_SOURCES))
+    _link(objs[len(SOURCES):], PROBE_LIB)
+    return _link(objs[:len(SOURCES)], LIB)
 
 
 def clean() -> None:

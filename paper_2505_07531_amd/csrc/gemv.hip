@@ -11,7 +11,9 @@
 //     that lanes on consecutive chunks hit different banks;
 //   * codes are decoded in registers (qx_device.h), one v_and_or_b32 per code
 //     pair, and multiplied with v_dot2_f32_f16 (exact fp16 products, fp32
-//     sums); uniform groups are scaled once per group;
+//     sums); uniform codes enter as M + q and the zero point is folded out
+//     once per group with sums over x formed while x is staged, so no
+//     instruction per pair subtracts it; groups are scaled once;
 //   * partial sums are reduced per row in a fixed order with DPP (no atomics;
 //     results are deterministic).
 //
@@ -39,23 +41,54 @@ constexpr int kXBlock = 272;                                   // LDS bytes per 
 // loads and wait for x alone.
 template <int XP>
 __device__ __forceinline__ void load_x(const uint16_t* __restrict__ x, int c0, int ct,
-                                       u32x4 (&xr)[XP]) {
+                                       u32x4 (&xr)[XP], int stride = kThreads) {
   const u32x4* src = reinterpret_cast<const u32x4*>(x) + (size_t)c0 * 16;
 #pragma unroll
   for (int i = 0; i < XP; ++i) {
-    const int p = min((int)threadIdx.x + i * kThreads, ct * 16 - 1);
+    const int p = min((int)threadIdx.x + i * stride, ct * 16 - 1);
     xr[i] = src[p];
   }
 }
 
-// Permute the loaded pieces into decoder pair order and store them in LDS.
-template <int BITS, int XP, bool EXACT = false>  // EXACT: every piece is in range
-__device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs) {
+// Sums over one 16-byte piece of x (8 natural-order values at chunk position
+// 8*pc) for the folded zero point of uniform groups: sum x and sum M x, M the
+// bias that the decoder adds to the code at each position (b = 4: 1024 at even,
+// 64 at odd positions; b = 3: 1024 for codes 0-47, 128 for 48-95, 16 above).
+// Products of fp16 values are exact in fp32.
+template <int BITS>
+__device__ __forceinline__ void piece_sums(const u32x4& v, int pc, float& sx, float& mx) {
+  const uint32_t one = 0x3C003C00u;  // (1, 1)
+  sx = dot2(v.w, one, dot2(v.z, one, dot2(v.y, one, dot2(v.x, one, 0.f))));
+  if (BITS == 4) {
+    const uint32_t m = 0x54006400u;  // (1024, 64)
+    mx = dot2(v.w, m, dot2(v.z, m, dot2(v.y, m, dot2(v.x, m, 0.f))));
+  } else {
+    mx = (pc < 6 ? 1024.f : pc < 12 ? 128.f : 16.f) * sx;
+  }
+}
+
+// Sum of v over aligned groups of N consecutive lanes (N = 4, 8, 16), in every lane.
+template <int N>
+__device__ __forceinline__ float lane_group_sum(float v) {
+  v = dpp_plus<0xB1, 0xF>(v);                    // quad_perm [1,0,3,2]
+  v = dpp_plus<0x4E, 0xF>(v);                    // quad_perm [2,3,0,1]
+  if constexpr (N >= 8) v = dpp_plus<0x141, 0xF>(v);   // row_half_mirror
+  if constexpr (N >= 16) v = dpp_plus<0x140, 0xF>(v);  // row_mirror
+  return v;
+}
+
+// Permute the loaded pieces into decoder pair order and store them in LDS
+// (piece p of the tile: chunk p / 16, values 8 (p % 16) ..). For uniform
+// groups, also store (sum M x, sum x) per group of the tile in gs; the pieces
+// of a group sit in consecutive lanes.
+template <int BITS, int KIND, int G, int XP, bool EXACT = false>  // EXACT: every piece is in range
+__device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs, float2* gs,
+                                        int stride = kThreads) {
 #pragma unroll
   for (int i = 0; i < XP; ++i) {
-    const int p = threadIdx.x + i * kThreads;
+    const int p = threadIdx.x + i * stride;
+    const u32x4 v = xr[i];
     if (EXACT || p < ct * 16) {
-      const u32x4 v = xr[i];
       u32x4 o;
       if (BITS == 4) {  // [x0 x1][x2 x3][x4 x5][x6 x7] -> [x0 x4][x1 x5][x2 x6][x3 x7]
         o.x = perm(v.z, v.x, 0x05040100u);
@@ -69,6 +102,14 @@ __device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs)
         o.w = perm(v.w, v.z, 0x07060302u);
       }
       *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
+    }
+    if constexpr (KIND == QX_UNIFORM) {
+      constexpr int PPG = G / 8;  // pieces per group
+      float sx, mx;
+      piece_sums<BITS>(v, p & 15, sx, mx);
+      sx = lane_group_sum<PPG>(sx);
+      mx = lane_group_sum<PPG>(mx);
+      if ((p & (PPG - 1)) == 0 && (EXACT || p < ct * 16)) gs[p / PPG] = make_float2(mx, sx);
     }
   }
 }
@@ -121,28 +162,36 @@ __device__ __forceinline__ uint32_t spare_sel(const Item<BITS, KIND, G>& it) {
   return u3_sel_spare<I>(it.d[I], it.d[8 + (I & 3)]);
 }
 
-// Partial dot product of one chunk with its x block (LDS, pair order).
+// Scale and zero point of a uniform group word: s * (acc - sum M x - z sum x),
+// with acc = sum (M + q) x over the group, is s * sum (q - z) x.
+__device__ __forceinline__ float fold_group(uint32_t word, float acc, float2 gsum) {
+  const float s = half_bits_to_float(word & 0xFFFFu), z = half_bits_to_float(word >> 16);
+  return s * (acc - gsum.x - z * gsum.y);
+}
+
+// Partial dot product of one chunk with its x block (LDS, pair order). Uniform
+// codes enter the products as M + q (no subtraction per pair); gs holds the
+// chunk's (sum M x, sum x) per group and fold_group takes the zero point out.
 template <int BITS, int KIND, int G>
 __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const char* xb,
-                                           const DecodeConsts& k) {
+                                           const float2* gs, const DecodeConsts& k) {
   constexpr int NG = 128 / G;
   const u32x4* xv = reinterpret_cast<const u32x4*>(xb);
   if constexpr (BITS == 4 && KIND == 0) {
     float part = 0.f;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const UniformGroup ug = uniform_group<4>(it.m[g]);
       float acc = 0.f;
 #pragma unroll
       for (int j = g * G / 8; j < (g + 1) * G / 8; ++j) {
         const u32x4 x = xv[j];
         const uint32_t D = it.d[j], Ds = D >> 8;
-        acc = dot2(hadd2((D & k.m000f) | k.mag1024, ug.z1024), x.x, acc);  // (0, 4)
-        acc = dot2(hadd2((D & k.m00f0) | k.mag64, ug.z64), x.y, acc);      // (1, 5)
-        acc = dot2(hadd2((Ds & k.m000f) | k.mag1024, ug.z1024), x.z, acc); // (2, 6)
-        acc = dot2(hadd2((Ds & k.m00f0) | k.mag64, ug.z64), x.w, acc);     // (3, 7)
+        acc = dot2((D & k.m000f) | k.mag1024, x.x, acc);   // (0, 4)
+        acc = dot2((D & k.m00f0) | k.mag64, x.y, acc);     // (1, 5)
+        acc = dot2((Ds & k.m000f) | k.mag1024, x.z, acc);  // (2, 6)
+        acc = dot2((Ds & k.m00f0) | k.mag64, x.w, acc);    // (3, 7)
       }
-      part += ug.s * acc;
+      part += fold_group(it.m[g], acc, gs[g]);
     }
     return part;
   } else if constexpr (BITS == 4 && KIND == 1) {
@@ -166,12 +215,8 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     return acc;
   } else if constexpr (BITS == 3 && KIND == 0) {
     float acc[NG];
-    UniformGroup ug[NG];
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      acc[g] = 0.f;
-      ug[g] = uniform_group<3>(it.m[g]);
-    }
+    for (int g = 0; g < NG; ++g) acc[g] = 0.f;
     // x dwords of code block t (codes 4t..4t+3): 2t = pair (0,2), 2t+1 = pair (1,3)
     const uint32_t* xd = reinterpret_cast<const uint32_t*>(xb);
 #pragma unroll
@@ -180,10 +225,10 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
       const int ga = (4 * i) / G, gb = (48 + 4 * i) / G;
       const u32x2 xa = *reinterpret_cast<const u32x2*>(xd + 2 * i);
       const u32x2 xb2 = *reinterpret_cast<const u32x2*>(xd + 2 * (12 + i));
-      acc[ga] = dot2(hadd2(p.a0, ug[ga].z1024), xa.x, acc[ga]);
-      acc[ga] = dot2(hadd2(p.a1, ug[ga].z1024), xa.y, acc[ga]);
-      acc[gb] = dot2(hadd2(p.b0, ug[gb].z128), xb2.x, acc[gb]);
-      acc[gb] = dot2(hadd2(p.b1, ug[gb].z128), xb2.y, acc[gb]);
+      acc[ga] = dot2(p.a0, xa.x, acc[ga]);
+      acc[ga] = dot2(p.a1, xa.y, acc[ga]);
+      acc[gb] = dot2(p.b0, xb2.x, acc[gb]);
+      acc[gb] = dot2(p.b1, xb2.y, acc[gb]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -198,14 +243,14 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
         case 6: spare_pairs<6>(it, k, s0, s1); break;
         default: spare_pairs<7>(it, k, s0, s1); break;
       }
-      const int gs = (96 + 4 * i) / G;
+      const int gg = (96 + 4 * i) / G;
       const u32x2 xs = *reinterpret_cast<const u32x2*>(xd + 2 * (24 + i));
-      acc[gs] = dot2(hadd2(s0, ug[gs].z16), xs.x, acc[gs]);
-      acc[gs] = dot2(hadd2(s1, ug[gs].z16), xs.y, acc[gs]);
+      acc[gg] = dot2(s0, xs.x, acc[gg]);
+      acc[gg] = dot2(s1, xs.y, acc[gg]);
     }
     float part = 0.f;
 #pragma unroll
-    for (int g = 0; g < NG; ++g) part += ug[g].s * acc[g];
+    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], acc[g], gs[g]);
     return part;
   } else {  // BITS == 3, codebook
     LutGroup<3> t[NG];
@@ -253,36 +298,37 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
 
 // K = 128*LPR with LPR in {32, 64}: a row's chunks fill LPR lanes of one wave, so
 // each row is reduced in registers with DPP and stored by one lane; no LDS
-// partials and no second barrier. Block = 4 waves = 4*(64/LPR) rows per round;
-// ROUNDS rounds per block, all loads issued up front.
-template <int BITS, int KIND, int G, int LPR, int ROUNDS>
-__global__ __launch_bounds__(kThreads) void gemv_wave_kernel(const char* __restrict__ packed,
-                                                              const uint16_t* __restrict__ x,
-                                                              uint16_t* __restrict__ y, int n) {
-  constexpr int C = LPR, RPW = 64 / LPR, RPB = 4 * RPW, XP = C * 16 / kThreads;
+// partials and no second barrier. A block has WPB waves and stages x once for
+// its WPB*64/LPR rows.
+template <int BITS, int KIND, int G, int LPR, int WPB>
+__global__ __launch_bounds__(64 * WPB) void gemv_wave_kernel(const char* __restrict__ packed,
+                                                             const uint16_t* __restrict__ x,
+                                                             uint16_t* __restrict__ y, int n) {
+  constexpr int C = LPR, NT = 64 * WPB, RPW = 64 / LPR, RPB = WPB * RPW;
+  constexpr int XP = (C * 16 + NT - 1) / NT;
   __shared__ __align__(16) char xs[C * kXBlock];
+  __shared__ float2 gs[KIND == QX_UNIFORM ? C * (128 / G) : 1];
   const int k = C * 128;
   const size_t meta_off = (size_t)n * k * BITS / 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c = lane & (LPR - 1);
-  const int row_base = blockIdx.x * (RPB * ROUNDS) + wave * RPW + lane / LPR;
+  const int row = blockIdx.x * RPB + wave * RPW + lane / LPR;
   const DecodeConsts kc = decode_consts();
 
   u32x4 xr[XP];
-  load_x<XP>(x, 0, C, xr);
-  Item<BITS, KIND, G> it[ROUNDS];
-#pragma unroll
-  for (int j = 0; j < ROUNDS; ++j)
-    load_item<BITS, KIND, G>(it[j], packed, meta_off, min(row_base + j * RPB, n - 1), c, C, k / G);
-  store_x<BITS, XP, true>(xr, C, xs);
+  load_x<XP>(x, 0, C, xr, NT);
+  Item<BITS, KIND, G> it;
+  load_item<BITS, KIND, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
+  store_x<BITS, KIND, G, XP, C * 16 % NT == 0>(xr, C, xs, gs, NT);
   __syncthreads();
-#pragma unroll
-  for (int j = 0; j < ROUNDS; ++j) {
-    const int row = row_base + j * RPB;
-    float v = chunk_dot<BITS, KIND, G>(it[j], xs + c * kXBlock, kc);
-    v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
-    if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
-  }
+  float v = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc);
+  v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
+  if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
+}
+
+// Byte offset of the group sums after C chunks of x and n floats of partials.
+__host__ __device__ constexpr int row_lds_gsum_offset(int C, int nfloats) {
+  return C * kXBlock + (nfloats * 4 + 7) / 8 * 8;
 }
 
 // K up to 88 chunks, any count: one (row, chunk) item per lane. The block has
@@ -301,6 +347,7 @@ __global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__
   const int rows = min(R, n - row0);
   char* xs = smem;                                             // C * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + C * kXBlock);  // R * C floats
+  float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(C, R * C));  // C * 128/G
   const DecodeConsts kc = decode_consts();
 
   u32x4 xr[XP];
@@ -311,28 +358,9 @@ __global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__
   const bool valid = r < rows;
   Item<BITS, KIND, G> it;
   load_item<BITS, KIND, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
-#pragma unroll
-  for (int i = 0; i < XP; ++i) {
-    const int p = threadIdx.x + i * nthreads;
-    if (p < C * 16) {
-      const u32x4 v = xr[i];
-      u32x4 o;
-      if (BITS == 4) {
-        o.x = perm(v.z, v.x, 0x05040100u);
-        o.y = perm(v.z, v.x, 0x07060302u);
-        o.z = perm(v.w, v.y, 0x05040100u);
-        o.w = perm(v.w, v.y, 0x07060302u);
-      } else {
-        o.x = perm(v.y, v.x, 0x05040100u);
-        o.y = perm(v.y, v.x, 0x07060302u);
-        o.z = perm(v.w, v.z, 0x05040100u);
-        o.w = perm(v.w, v.z, 0x07060302u);
-      }
-      *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
-    }
-  }
+  store_x<BITS, KIND, G, XP>(xr, C, xs, gs, nthreads);
   __syncthreads();
-  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, kc);
+  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc);
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int rr = wave; rr < rows; rr += nthreads >> 6) {
@@ -361,6 +389,7 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
   char* xs = smem;                                              // CT * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + CT * kXBlock);  // R * CT floats
+  float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(CT, R * CT));  // CT * 128/G
   const DecodeConsts kc = decode_consts();
 
   float acc[ITEMS];
@@ -385,11 +414,11 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
                                c0 + min(cl[j], ct - 1), C, G_row);
     }
     if (c0 > 0) __syncthreads();  // previous tile's x no longer read
-    store_x<BITS, XP>(xr, ct, xs);
+    store_x<BITS, KIND, G, XP>(xr, ct, xs, gs);
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j)
-      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock, kc);
+      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock, gs + cl[j] * (128 / G), kc);
   }
 
 #pragma unroll
@@ -407,21 +436,12 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
   }
 }
 
-// Rows per block and items per lane of the tile kernel for an n x k matrix.
-#ifndef QX_GEMV_ROUNDS
-#define QX_GEMV_ROUNDS 0  // 0: choose per shape
-#endif
 #ifndef QX_GEMV_TILE_ROWS
 #define QX_GEMV_TILE_ROWS 8
 #endif
-// Rounds per block of the wave kernel. One round (one chunk per lane) measured
-// fastest at every decoder shape, even when the grid exceeds one resident
-// generation of blocks: more resident waves hide latency better than more
-// independent loads per lane.
-static int wave_rounds(int n, int rpb) {
-  (void)n; (void)rpb;
-  return QX_GEMV_ROUNDS > 0 ? QX_GEMV_ROUNDS : 1;
-}
+#ifndef QX_GEMV_WPB
+#define QX_GEMV_WPB 4  // waves per block of the wave kernel
+#endif
 
 // Rows per block and block size of the row kernel for C chunks per row: among
 // blocks of at least 256 threads (x is staged once per block), the R whose R*C
@@ -460,7 +480,7 @@ static void launch_gemv_tile(const qx_desc* d, const char* p, const uint16_t* x,
   gemv_tile_shape(d->n, d->k, &R, &items);
   const int C = d->k / 128;
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
-  const size_t lds = (size_t)CT * kXBlock + (size_t)R * CT * sizeof(float);
+  const size_t lds = (size_t)row_lds_gsum_offset(CT, R * CT) + (size_t)CT * (128 / G) * sizeof(float2);
   const dim3 grid((d->n + R - 1) / R), block(kThreads);
   const int xp = (CT * 16 + kThreads - 1) / kThreads;  // x pieces per thread: 1..6
 #define QX_GEMV_LAUNCH(I, XP) \
@@ -494,32 +514,20 @@ static int launch_gemv_t(const qx_desc* d, const void* packed, const uint16_t* x
   const char* p = static_cast<const char*>(packed);
   const int C = d->k / 128;
   if (C == 32 || C == 64) {
-    const int rpb = C == 32 ? 8 : 4;  // rows per block per round
-    const int rounds = wave_rounds(d->n, rpb);
-    const unsigned blocks = (unsigned)((d->n + rpb * rounds - 1) / (rpb * rounds));
-#define QX_WAVE_LAUNCH(L, RD) \
-  hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, L, RD>), dim3(blocks), dim3(kThreads), 0, s, p, x, y, d->n)
-    if (C == 32) {
-      switch (rounds) {
-        case 1: QX_WAVE_LAUNCH(32, 1); break;
-        case 2: QX_WAVE_LAUNCH(32, 2); break;
-        case 3: QX_WAVE_LAUNCH(32, 3); break;
-        default: QX_WAVE_LAUNCH(32, 4); break;
-      }
-    } else {
-      switch (rounds) {
-        case 1: QX_WAVE_LAUNCH(64, 1); break;
-        case 2: QX_WAVE_LAUNCH(64, 2); break;
-        case 3: QX_WAVE_LAUNCH(64, 3); break;
-        default: QX_WAVE_LAUNCH(64, 4); break;
-      }
-    }
-#undef QX_WAVE_LAUNCH
+    // one (row, chunk) item per lane: more resident waves measured faster than more
+    // items per lane at every decoder shape
+    constexpr int WPB = QX_GEMV_WPB;
+    const int rpb = WPB * 64 / C;
+    const unsigned blocks = (unsigned)((d->n + rpb - 1) / rpb);
+    if (C == 32)
+      hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, 32, WPB>), dim3(blocks), dim3(64 * WPB), 0, s, p, x, y, d->n);
+    else
+      hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, 64, WPB>), dim3(blocks), dim3(64 * WPB), 0, s, p, x, y, d->n);
   } else if (C <= kMaxTileChunks) {
     int R, threads;
     gemv_row_shape(C, &R, &threads);
     const unsigned blocks = (unsigned)((d->n + R - 1) / R);
-    const size_t lds = (size_t)C * kXBlock + (size_t)R * C * sizeof(float);
+    const size_t lds = (size_t)row_lds_gsum_offset(C, R * C) + (size_t)C * (128 / G) * sizeof(float2);
     const int xp = (C * 16 + threads - 1) / threads;
 #define QX_ROW_LAUNCH(XP) \
   hipLaunchKernelGGL((gemv_row_kernel<BITS, KIND, G, XP>), dim3(blocks), dim3(threads), lds, s, p, x, y, d->n, d->k, R)

@@ -67,27 +67,6 @@ constexpr uint32_t kMagic1024 = 0x64006400u;
 constexpr uint32_t kMagic128 = 0x58005800u;
 constexpr uint32_t kMagic16 = 0x4C004C00u;
 
-// Per-group constants of a uniform group: scale, and -(M + z) pairs for the three
-// field positions.
-struct UniformGroup {
-  float s;
-  uint32_t z1024, z128, z64, z16;
-};
-template <int BITS>
-__device__ __forceinline__ UniformGroup uniform_group(uint32_t word) {
-  UniformGroup g;
-  g.s = half_bits_to_float(word & 0xFFFFu);
-  const float z = half_bits_to_float(word >> 16);
-  g.z1024 = splat_half(-(1024.0f + z));
-  if (BITS == 3) {
-    g.z128 = splat_half(-(128.0f + z));
-    g.z16 = splat_half(-(16.0f + z));
-  } else {
-    g.z64 = splat_half(-(64.0f + z));
-  }
-  return g;
-}
-
 // Register byte tables of one codebook group: lo[t] / hi[t] hold the low / high
 // bytes of entries 4t..4t+3 (t < 2^b / 4).
 template <int BITS>

@@ -16,14 +16,40 @@ import paper_2505_07531_amd as qx
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def test_library_exports_every_declared_symbol():
-    with open(os.path.join(ROOT, "include", "qx.h")) as f:
+def _declared(header, prefix):
+    with open(os.path.join(ROOT, "include", header)) as f:
         hdr = f.read()
-    declared = set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(qx_\w+)\s*\(", hdr, re.M))
+    return set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(" + prefix + r"\w+)\s*\(", hdr, re.M))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared("qx.h", "qx_")
     assert {"qx_pack_layout", "qx_dequant", "qx_gemv", "qx_gemm", "qx_status_str"} <= declared
     lib = ctypes.CDLL(qx.LIB_PATH if os.path.exists(qx.LIB_PATH) else qx.build())
     for name in sorted(declared):
         assert hasattr(lib, name), name
+
+
+def test_every_header_is_checked_against_its_library():
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == ["qx.h", "qx_probe.h"]
+
+
+def test_probe_library_exports_and_rejects_bad_arguments():
+    from paper_2505_07531_amd import probe
+    declared = _declared("qx_probe.h", "qxp_")
+    assert declared == {"qxp_read", "qxp_empty"}
+    lib = probe.load()
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    # each call fails an argument check, so nothing is launched
+    assert lib.qxp_read(None, 16, None, None) == -1
+    assert lib.qxp_read(64, 0, 64, None) == -1      # empty read
+    assert lib.qxp_read(64, 24, 64, None) == -1     # not a multiple of 16
+    assert lib.qxp_read(8, 16, 64, None) == -1      # src not 16-byte aligned
+    assert lib.qxp_empty(0, 64, None) == -1
+    assert lib.qxp_empty((1 << 20) + 1, 64, None) == -1
+    assert lib.qxp_empty(1, None, None) == -1
 
 
 def _random_quant(n, k, bits, group, kind, seed):
