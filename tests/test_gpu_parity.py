@@ -86,6 +86,7 @@ def test_gemv_matches_oracle(gpu, fmt, shape):
     y = pw.gemv(to_dev(x)).cpu().numpy()
     ref = oracle.gemv(_ref_w16(q), x)
     err = oracle.normwise_rel_err(y, ref)
+    print(f"gemv {fmt} {shape} normwise rel err {err:.3e}")
     assert err <= TOL, err
 
 
@@ -164,7 +165,7 @@ def test_gemm_prefill_shapes(gpu, m, name):
 
 # activation tiles mapped to XCDs with padding blocks, single-chunk rows, chunk counts
 # that leave K-split waves idle in the last round
-GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40)]
+GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40), (1, 640, 17)]
 
 
 @pytest.mark.parametrize("fmt", [(3, 0, 64), (4, 0, 128), (3, 1, 32), (4, 1, 32)], ids=_fmt_id)
@@ -191,3 +192,73 @@ def test_gemm_rows_equal_gemv_within_tolerance(gpu):
     for r in range(9):
         y = pw.gemv(to_dev(X[r])).cpu().numpy()
         assert oracle.normwise_rel_err(Y[r], y.astype(np.float64)) <= 2 * TOL
+
+
+# ---- maximum sizes and degenerate inputs
+
+K_MAX = 1 << 20  # largest k the interface accepts
+EDGE_FORMATS = [(3, 0, 64), (4, 0, 128), (3, 1, 128), (4, 1, 32)]
+
+
+@pytest.mark.parametrize("fmt", EDGE_FORMATS, ids=_fmt_id)
+def test_max_k_dequant_and_gemv(gpu, fmt):
+    qx = gpu
+    bits, kind, g = fmt
+    print(f"k = 2^20 {fmt}", flush=True)
+    q = random_quant(3, K_MAX, bits, g, kind, seed=bits + g)
+    pw = _pack(qx, q)
+    w16 = _ref_w16(q)
+    assert np.array_equal(pw.dequant(qx.QX_OUT_CODES).cpu().numpy(), q.codes)
+    assert np.array_equal(pw.dequant(qx.QX_OUT_F16).cpu().numpy().view(np.uint16), w16.view(np.uint16))
+    x = activations(K_MAX, seed=7)
+    y = pw.gemv(to_dev(x)).cpu().numpy()
+    assert oracle.normwise_rel_err(y, oracle.gemv(w16, x)) <= TOL
+    X = activations(K_MAX, seed=8, m=3)
+    Y = pw.gemm(to_dev(X)).cpu().numpy()
+    ref = oracle.gemm(X, w16)
+    for r in range(3):
+        assert oracle.normwise_rel_err(Y[r], ref[r]) <= TOL, r
+
+
+def test_max_m_gemm(gpu):
+    qx = gpu
+    m, n, k = 65536, 20, 256  # the largest m the interface accepts
+    print("gemm m = 65536", flush=True)
+    q = realistic_quant(n, k, 3, 64, 0, seed=3)
+    X = activations(k, seed=9, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    ref = oracle.gemm(X, _ref_w16(q))
+    err = max(oracle.normwise_rel_err(Y[r], ref[r]) for r in range(0, m, 97))
+    assert err <= TOL, err
+    assert oracle.normwise_rel_err(Y[m - 1], ref[m - 1]) <= TOL
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+def test_zero_weights_give_zero(gpu, fmt):
+    """Every code at the zero point (uniform) or every table entry +0 (codebook): W' = 0
+    exactly. Dequant and GEMM (which multiply W') give exact zeros. The uniform GEMV folds
+    the zero point out per group, s * (sum (M+q) x - sum M x - z sum x), so its zero comes
+    out of fp32 rounding of those sums: bounded here by 2e-3 of what one code step per
+    weight gives, sum_k |s| |x_k|, per row (the normwise scale of the parity bound)."""
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = 70, 11008
+    q = random_quant(n, k, bits, g, kind, seed=17)
+    if kind == 0:
+        zi = np.random.default_rng(1).integers(0, 2**bits, (n, k // g))
+        q.zeros = zi.astype(np.float16).view(np.uint16)
+        q.codes = np.repeat(zi, g, axis=1).astype(np.uint8)
+    else:
+        q.codebook = np.zeros_like(q.codebook)
+    pw = _pack(qx, q)
+    assert not np.any(pw.dequant(qx.QX_OUT_F16).cpu().numpy().astype(np.float64))
+    x = activations(k, seed=2)
+    y = pw.gemv(to_dev(x)).cpu().numpy().astype(np.float64)
+    if kind == 0:
+        s = np.abs(q.scales.view(np.float16).astype(np.float64))
+        scale = (s * np.abs(x.astype(np.float64)).reshape(k // g, g).sum(axis=1)).sum(axis=1)
+        assert np.all(np.abs(y) <= TOL * scale), np.max(np.abs(y) / scale)
+    else:
+        assert not np.any(y)
+    X = activations(k, seed=3, m=5)
+    assert not np.any(pw.gemm(to_dev(X)).cpu().numpy().astype(np.float64))
