@@ -440,7 +440,8 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16
                      0, s, p, X, Y, d->n, d->k, m, nx, my);
 }
 
-// Tile shape per activation row count. Small m is bound by streaming the codes:
+// Tile shape per activation row count (from a sweep of MT, NT, KS, S, DX on the
+// 3-bit g64 MLP shapes at m = 16, 64, 512). Small m is bound by streaming the codes:
 // one 16-row activation tile, 16 weight rows per block and the chunks of a row
 // split over the four waves, so that the grid has enough blocks. Larger m gets
 // larger activation tiles so that each decoded weight feeds more MFMAs; with
@@ -456,11 +457,11 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint
   const int cfg = QX_GEMM_CFG > 0 ? QX_GEMM_CFG : m <= 16 ? 1 : m <= 64 ? 2 : 4;
   switch (cfg) {
     case 1:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 4, 4>(d, p, m, X, Y, s);
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 2, 2>(d, p, m, X, Y, s);
       else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1>(d, p, m, X, Y, s);
       break;
     case 2:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 4, 2>(d, p, m, X, Y, s);
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1>(d, p, m, X, Y, s);
       else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
       break;
     default:
