@@ -326,6 +326,70 @@ __global__ __launch_bounds__(64 * WPB) void gemv_wave_kernel(const char* __restr
   if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
 }
 
+// Codebook 3-bit, group 128, k = 128*32, for matrices with few rows: two lanes
+// per chunk, one row per wave, so that each wave carries half the decode work
+// and a SIMD interleaves twice as many waves while the codes arrive. Lane l
+// takes chunk l % 32; lanes 0-31 decode the fields in bits 0-2 (codes 0-47) and
+// the spare codes of dwords 0-3, lanes 32-63 the fields in bits 3-5 (codes
+// 48-95) and the spare codes of dwords 4-7. Both run the same instructions: the
+// second half loads slice 1 into the registers the first half fills with slice
+// 0 and vice versa, and the field shift, spare bit and x offsets are per lane.
+template <int WPB>
+__global__ __launch_bounds__(64 * WPB) void gemv_cb3_half_kernel(const char* __restrict__ packed,
+                                                                 const uint16_t* __restrict__ x,
+                                                                 uint16_t* __restrict__ y, int n) {
+  constexpr int C = 32, NT = 64 * WPB, XP = (C * 16 + NT - 1) / NT;
+  __shared__ __align__(16) char xs[C * kXBlock];
+  float2* no_gs = nullptr;  // codebook groups need no sums over x
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & 31, h = lane >> 5;
+  const int row = blockIdx.x * WPB + wave;
+  const size_t meta_off = (size_t)n * C * 128 * 3 / 8;
+
+  u32x4 xr[XP];
+  load_x<XP>(x, 0, C, xr, NT);
+  const int r = min(row, n - 1);
+  const u32x4* code = reinterpret_cast<const u32x4*>(packed) + ((size_t)r * 3 * C + c);
+  const u32x4 s0 = __builtin_nontemporal_load(code + (size_t)h * C);        // slice h
+  const u32x4 s1 = __builtin_nontemporal_load(code + (size_t)(1 - h) * C);  // slice 1 - h
+  const u32x4 s2 = __builtin_nontemporal_load(code + (size_t)2 * C);
+  const u32x4 tb = __builtin_nontemporal_load(
+      reinterpret_cast<const u32x4*>(packed + meta_off + ((size_t)r * C + c) * 16));
+  store_x<3, QX_CODEBOOK, 128, XP, C * 16 % NT == 0>(xr, C, xs, no_gs, NT);
+  __syncthreads();
+
+  const uint32_t m[4] = {tb.x, tb.y, tb.z, tb.w};
+  const LutGroup<3> t = lut_group<3>(m);
+  const uint32_t sh = 3u * h;                     // field: bits 0-2 or 3-5 of each byte
+  const uint32_t ssh = 4u + h;                    // spare bit 2: bit 6 or 7 of H
+  const char* xc = xs + c * kXBlock;
+  // x blocks (4 codes, 8 bytes) of register group R0 / R1 / R2 and of the spare codes
+  const int xo0 = h ? 8 * 16 : 0, xo1 = h ? 8 * 12 : 8 * 4, xo2 = h ? 8 * 20 : 8 * 8;
+  const int xos = h ? 8 * 28 : 8 * 24;
+  const uint32_t R[12] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w, s2.x, s2.y, s2.z, s2.w};
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    const int xo = (i < 4 ? xo0 : i < 8 ? xo1 : xo2) + 8 * (i & 3);
+    uint32_t p02, p13;
+    lut3_pairs(t, (R[i] >> sh) & 0x07070707u, p02, p13);
+    const u32x2 xv = *reinterpret_cast<const u32x2*>(xc + xo);
+    acc = dot2(p02, xv.x, acc);
+    acc = dot2(p13, xv.y, acc);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {  // spare codes of the dword in R0[i]; bit 2 in R2[i]
+    const uint32_t S = ((R[i] >> 6) & 0x03030303u) | ((R[8 + i] >> ssh) & 0x04040404u);
+    uint32_t p02, p13;
+    lut3_pairs(t, S, p02, p13);
+    const u32x2 xv = *reinterpret_cast<const u32x2*>(xc + xos + 8 * i);
+    acc = dot2(p02, xv.x, acc);
+    acc = dot2(p13, xv.y, acc);
+  }
+  const float v = wave_sum(acc);
+  if (lane == 63 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
+}
+
 // Byte offset of the group sums after C chunks of x and n floats of partials.
 __host__ __device__ constexpr int row_lds_gsum_offset(int C, int nfloats) {
   return C * kXBlock + (nfloats * 4 + 7) / 8 * 8;
@@ -439,6 +503,9 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
 #ifndef QX_GEMV_TILE_ROWS
 #define QX_GEMV_TILE_ROWS 8
 #endif
+#ifndef QX_GEMV_HALF_MAX_N
+#define QX_GEMV_HALF_MAX_N 8192  // rows up to which codebook-3 g128 rows of 32 chunks take two lanes per chunk
+#endif
 #ifndef QX_GEMV_WPB
 #define QX_GEMV_WPB 4  // waves per block of the wave kernel
 #endif
@@ -519,7 +586,9 @@ static int launch_gemv_t(const qx_desc* d, const void* packed, const uint16_t* x
     constexpr int WPB = QX_GEMV_WPB;
     const int rpb = WPB * 64 / C;
     const unsigned blocks = (unsigned)((d->n + rpb - 1) / rpb);
-    if (C == 32)
+    if (BITS == 3 && KIND == QX_CODEBOOK && G == 128 && C == 32 && d->n <= QX_GEMV_HALF_MAX_N)
+      hipLaunchKernelGGL((gemv_cb3_half_kernel<8>), dim3((d->n + 7) / 8), dim3(512), 0, s, p, x, y, d->n);
+    else if (C == 32)
       hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, 32, WPB>), dim3(blocks), dim3(64 * WPB), 0, s, p, x, y, d->n);
     else
       hipLaunchKernelGGL((gemv_wave_kernel<BITS, KIND, G, 64, WPB>), dim3(blocks), dim3(64 * WPB), 0, s, p, x, y, d->n);
