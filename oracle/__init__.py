@@ -16,11 +16,18 @@ Table 1):
   y[n]    = sum_k W'[n,k] * x[k]                      in fp64
   Y[m,n]  = sum_k X[m,k] * W'[n,k]                    in fp64
 
+The paper's own 4-bit format, Q4X (Section 3.2: a per-matrix codebook of 4 x
+16 centroids, per group of 64 a scale and a 2-bit sub-codebook selector), has
+its layout and dequantization in ``q4x``:
+
+  W'[n,k] = fp16_RNE( s[n,j] * CB[sel[n,j]][q[n,k]] ),  j = k // 64
+
 Modules: ``layout`` (pack/unpack of the packed layout), ``dequant``,
 ``matmul`` (fp64 products and the error metric), ``formats`` (sizes and
-bits-per-weight).
+bits-per-weight), ``q4x``.
 """
 from .layout import chunk_bit_positions, pack, unpack  # noqa: F401
 from .dequant import dequant, dequant_packed  # noqa: F401
 from .matmul import gemv, gemm, normwise_rel_err  # noqa: F401
 from .formats import packed_size, bits_per_weight  # noqa: F401
+from . import q4x  # noqa: F401

@@ -68,14 +68,13 @@ def _check(n, k, bits, group, kind):
         raise ValueError("k must be a positive multiple of 128 and of the group size")
 
 
-def pack(codes, bits, group, kind, scales=None, zeros=None, codebook=None) -> np.ndarray:
-    """Packed blob (uint8) of codes [n][k] and the per-group tables (binary16 bit patterns)."""
+def pack_code_region(codes, bits) -> np.ndarray:
+    """Codes region (uint8, n*k*b/8 bytes) of codes [n][k]."""
     codes = np.asarray(codes, dtype=np.uint8)
     n, k = codes.shape
-    _check(n, k, bits, group, kind)
     if np.any(codes >= (1 << bits)):
         raise ValueError("code out of range")
-    C, G = k // CHUNK, k // group
+    C = k // CHUNK
     pos = chunk_bit_positions(bits)
     chunks = codes.reshape(n, C, CHUNK)
     bitarr = np.zeros((n, C, CHUNK * bits), dtype=np.uint8)
@@ -84,7 +83,32 @@ def pack(codes, bits, group, kind, scales=None, zeros=None, codebook=None) -> np
             bitarr[:, :, pos[i, t]] = (chunks[:, :, i] >> t) & 1
     chunk_bytes = np.packbits(bitarr, axis=-1, bitorder="little")          # [n, C, 16b]
     planes = chunk_bytes.reshape(n, C, bits, 16).transpose(0, 2, 1, 3)      # [n, b, C, 16]
-    code_region = np.ascontiguousarray(planes).reshape(-1)
+    return np.ascontiguousarray(planes).reshape(-1)
+
+
+def unpack_code_region(blob, n, k, bits) -> np.ndarray:
+    """Codes [n][k] (uint8) from the first n*k*b/8 bytes of a blob."""
+    blob = np.asarray(blob, dtype=np.uint8).reshape(-1)
+    C = k // CHUNK
+    ncode = n * k * bits // 8
+    planes = blob[:ncode].reshape(n, bits, C, 16).transpose(0, 2, 1, 3)   # [n, C, b, 16]
+    chunk_bytes = np.ascontiguousarray(planes).reshape(n, C, 16 * bits)
+    bitarr = np.unpackbits(chunk_bytes, axis=-1, bitorder="little")       # [n, C, 128b]
+    pos = chunk_bit_positions(bits)
+    codes = np.zeros((n, C, CHUNK), dtype=np.uint8)
+    for i in range(CHUNK):
+        for t in range(bits):
+            codes[:, :, i] |= bitarr[:, :, pos[i, t]] << t
+    return codes.reshape(n, k)
+
+
+def pack(codes, bits, group, kind, scales=None, zeros=None, codebook=None) -> np.ndarray:
+    """Packed blob (uint8) of codes [n][k] and the per-group tables (binary16 bit patterns)."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    n, k = codes.shape
+    _check(n, k, bits, group, kind)
+    G = k // group
+    code_region = pack_code_region(codes, bits)
     if kind == UNIFORM:
         s = np.asarray(scales, dtype=np.uint16).reshape(n, G).astype(np.uint32)
         z = np.asarray(zeros, dtype=np.uint16).reshape(n, G).astype(np.uint32)
@@ -103,17 +127,9 @@ def unpack(blob, n, k, bits, group, kind):
     """
     _check(n, k, bits, group, kind)
     blob = np.asarray(blob, dtype=np.uint8).reshape(-1)
-    C, G = k // CHUNK, k // group
+    G = k // group
     ncode = n * k * bits // 8
-    planes = blob[:ncode].reshape(n, bits, C, 16).transpose(0, 2, 1, 3)   # [n, C, b, 16]
-    chunk_bytes = np.ascontiguousarray(planes).reshape(n, C, 16 * bits)
-    bitarr = np.unpackbits(chunk_bytes, axis=-1, bitorder="little")       # [n, C, 128b]
-    pos = chunk_bit_positions(bits)
-    codes = np.zeros((n, C, CHUNK), dtype=np.uint8)
-    for i in range(CHUNK):
-        for t in range(bits):
-            codes[:, :, i] |= bitarr[:, :, pos[i, t]] << t
-    codes = codes.reshape(n, k)
+    codes = unpack_code_region(blob, n, k, bits)
     meta = blob[ncode:ncode + n * G * _meta_bytes_per_group(bits, kind)]
     if kind == UNIFORM:
         words = meta.view("<u4").reshape(n, G)

@@ -25,7 +25,7 @@ _SRC = os.path.join(_HERE, "_gen.cpp")
 _LIB = os.path.join(_HERE, "_libqxinputs.so")
 
 DIST = {"normal": 0, "laplace": 1, "t4": 2}
-UNIFORM, CODEBOOK = 0, 1
+UNIFORM, CODEBOOK, Q4X = 0, 1, 2
 
 
 def build(force: bool = True) -> str:
@@ -62,6 +62,10 @@ def lib():
         L.qxi_quantize_uniform.restype = c_int
         L.qxi_quantize_codebook.argtypes = [P, i64, i64, c_int, c_int, c_int, P, P, P, P, c_int]
         L.qxi_quantize_codebook.restype = c_int
+        L.qxi_q4x_histograms.argtypes = [P, i64, P, P, c_int]
+        L.qxi_q4x_histograms.restype = c_int
+        L.qxi_q4x_assign.argtypes = [P, i64, P, P, P, P, c_int]
+        L.qxi_q4x_assign.restype = c_int
         _lib = L
     return _lib
 
@@ -140,7 +144,9 @@ class QuantWeight:
     codes   uint8 [n][k], each < 2**bits
     scales  uint16 [n][k/group] binary16 bits   (uniform only)
     zeros   uint16 [n][k/group] binary16 bits, integer-valued (uniform only)
-    codebook uint16 [n][k/group][2**bits] binary16 bits (codebook only)
+    codebook uint16 [n][k/group][2**bits] binary16 bits (codebook only);
+             for Q4X (kind 2) the matrix's [4][16] codebook
+    selectors uint8 [n][k/64], each < 4 (Q4X only)
     """
     n: int
     k: int
@@ -152,13 +158,16 @@ class QuantWeight:
     zeros: Optional[np.ndarray] = None
     codebook: Optional[np.ndarray] = None
     meta: dict = field(default_factory=dict)
+    selectors: Optional[np.ndarray] = None
 
     def rows(self, r0: int, r1: int) -> "QuantWeight":
         sl = slice(r0, r1)
+        per_matrix = self.kind == Q4X  # one codebook for all rows
         return QuantWeight(r1 - r0, self.k, self.bits, self.group, self.kind, self.codes[sl],
                            None if self.scales is None else self.scales[sl],
                            None if self.zeros is None else self.zeros[sl],
-                           None if self.codebook is None else self.codebook[sl], dict(self.meta))
+                           None if self.codebook is None else (self.codebook if per_matrix else self.codebook[sl]),
+                           dict(self.meta), None if self.selectors is None else self.selectors[sl])
 
 
 def quantize_uniform(w: np.ndarray, bits: int, group: int) -> QuantWeight:

@@ -299,4 +299,61 @@ int qxi_quantize_codebook(const float* w, int64_t n, int64_t k, int bits, int g,
   return bad ? -2 : 0;
 }
 
+// Q4X (groups of 64, a 4 x 16 binary16 codebook): per group, the 32-bin histogram
+// over [-1, 1] of w / s16 (fractions), and, given the codebook, the nearest level
+// fp16(s16 * CB[t][e]) of every weight for each sub-codebook t (ties to the lowest
+// index) and the sub-codebook of least squared error (ties to the lowest t).
+int qxi_q4x_histograms(const float* w, int64_t ngroups, const uint16_t* s16, double* hist,
+                       int threads) {
+#pragma omp parallel for num_threads(threads) schedule(static)
+  for (int64_t g = 0; g < ngroups; ++g) {
+    const double s = half_to_double(s16[g]);
+    double* h = hist + g * 32;
+    for (int b = 0; b < 32; ++b) h[b] = 0.0;
+    for (int i = 0; i < 64; ++i) {
+      const double u = (double)w[g * 64 + i] / s;
+      int b = (int)std::floor((u + 1.0) * 16.0);
+      b = b < 0 ? 0 : (b > 31 ? 31 : b);
+      h[b] += 1.0 / 64.0;
+    }
+  }
+  return 0;
+}
+
+int qxi_q4x_assign(const float* w, int64_t ngroups, const uint16_t* s16, const uint16_t* cb,
+                   uint8_t* codes, uint8_t* sel, int threads) {
+#pragma omp parallel for num_threads(threads) schedule(static)
+  for (int64_t g = 0; g < ngroups; ++g) {
+    const double s = half_to_double(s16[g]);
+    double best_err = INFINITY;
+    uint8_t best_q[64];
+    int best_t = 0;
+    for (int t = 0; t < 4; ++t) {
+      double lv[16];
+      for (int e = 0; e < 16; ++e) lv[e] = half_to_double(double_to_half(s * half_to_double(cb[16 * t + e]), 0));
+      double err = 0.0;
+      uint8_t q[64];
+      for (int i = 0; i < 64; ++i) {
+        const double x = (double)w[g * 64 + i];
+        int best = 0;
+        double bd = std::fabs(x - lv[0]);
+        for (int e = 1; e < 16; ++e) {
+          const double d = std::fabs(x - lv[e]);
+          if (d < bd) { bd = d; best = e; }
+        }
+        q[i] = (uint8_t)best;
+        err += bd * bd;
+      }
+      if (err < best_err) {
+        best_err = err;
+        best_t = t;
+        for (int i = 0; i < 64; ++i) best_q[i] = q[i];
+      }
+    }
+    sel[g] = (uint8_t)best_t;
+    for (int i = 0; i < 64; ++i) codes[g * 64 + i] = best_q[i];
+  }
+  return 0;
+}
+
 }  // extern "C"

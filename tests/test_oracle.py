@@ -9,6 +9,7 @@ import pytest
 
 import oracle
 import qx_inputs as qi
+import qx_inputs.configs  # noqa: F401  (qi.configs)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
