@@ -41,6 +41,18 @@
  *   Metadata region at offset n*k*b/8:
  *     uniform : uint32 per (row, group) at (n*G + j)*4 = scale | zero << 16.
  *     codebook: 2^b fp16 entries per (row, group) at (n*G + j)*2^(b+1).
+ *
+ * Q4X (the paper's own 4-bit format, Section 3.2, Q4X item, and the Figure 3
+ * captions): one codebook of 64 fp16 centroids per matrix, as 4 sub-codebooks
+ * of 16; per group of g = 64 weights an fp16 scale s, a 2-bit selector t and
+ * 64 4-bit indices q; W' = fp16_RNE(s * CB[t][q]); 4 + 18/64 bits per weight.
+ * Blob (b = 4, W = ceil(G/16) selector words per row):
+ *   codes     offset 0: the 4-bit codes region above, n*k/2 bytes;
+ *   scales    offset S0 = n*k/2: fp16 per (row, group) at S0 + (n*G + j)*2;
+ *   selectors offset L0 = S0 + n*G*2: uint32 words, t of group j in bits
+ *             2*(j%16), 2*(j%16)+1 of word L0 + (n*W + j/16)*4; other bits 0;
+ *   codebook  offset B0 = L0 + n*W*4 rounded up to a multiple of 16: entry e
+ *             of sub-codebook t at B0 + (16*t + e)*2; total B0 + 128 bytes.
  */
 #ifndef QX_H_
 #define QX_H_
@@ -55,7 +67,7 @@ extern "C" {
 /* HIP's stream handle (the same declaration as hip_runtime_api.h). */
 typedef struct ihipStream_t* hipStream_t;
 
-enum { QX_UNIFORM = 0, QX_CODEBOOK = 1 };    /* qx_desc.kind */
+enum { QX_UNIFORM = 0, QX_CODEBOOK = 1, QX_Q4X = 2 };  /* qx_desc.kind */
 enum { QX_OUT_F16 = 0, QX_OUT_CODES = 1 };   /* qx_dequant out_kind */
 
 enum {
@@ -70,9 +82,10 @@ enum {
  * Descriptor of one quantized matrix.
  *   n     rows (output features), n >= 0
  *   k     reduction length, a positive multiple of 128 (at most 1 << 20)
- *   bits  code width b: 3 or 4
- *   group g: 32, 64 or 128
- *   kind  QX_UNIFORM or QX_CODEBOOK
+ *   bits  code width b: 3 or 4 (4 for QX_Q4X)
+ *   group g: 32, 64 or 128 (64 for QX_Q4X)
+ *   kind  QX_UNIFORM, QX_CODEBOOK or QX_Q4X; a QX_Q4X descriptor with other
+ *         bits or group is malformed (QX_E_ARG)
  *   flags must be 0
  */
 typedef struct {
@@ -95,17 +108,38 @@ typedef struct {
  * All pointers are host pointers. Pure and synchronous; returns QX_E_ARG for
  * a bad descriptor, a missing table, an out-of-range code or zero-point or a
  * non-finite scale, and QX_E_SIZE when cap < *packed_size (nothing written).
+ * QX_Q4X descriptors are packed by qx_pack_q4x (QX_E_ARG here).
  */
 int qx_pack_layout(const qx_desc* d, const uint8_t* codes, const uint16_t* scales,
                    const uint16_t* zeros, const uint16_t* codebook, void* packed, size_t cap,
                    size_t* packed_size);
 
 /*
+ * qx_pack_q4x -- write the packed blob of one Q4X matrix (host).
+ * Passage: Section 3.2, Q4X item (per group of 64 a 2-byte scale, a 2-bit
+ * codebook index and 64 4-bit centroid indices; 64 centroids per matrix in 4
+ * groups of 16), and the Figure 3a/3b captions.
+ *   d          descriptor with kind QX_Q4X, bits 4, group 64.
+ *   codes      uint8 [n][k] row-major, each < 16.
+ *   scales     fp16 [n][k/64]; any values (W' is their IEEE product).
+ *   selectors  uint8 [n][k/64], each < 4.
+ *   codebook   fp16 [4][16]: sub-codebook t, entry e at [t][e]; any values.
+ *   packed, cap, packed_size as for qx_pack_layout.
+ * All pointers are host pointers. Pure and synchronous; returns QX_E_ARG for a
+ * descriptor of another kind, a missing input or an out-of-range code or
+ * selector, and QX_E_SIZE when cap < *packed_size (nothing written).
+ */
+int qx_pack_q4x(const qx_desc* d, const uint8_t* codes, const uint16_t* scales,
+                const uint8_t* selectors, const uint16_t* codebook, void* packed, size_t cap,
+                size_t* packed_size);
+
+/*
  * qx_dequant -- expand a packed blob into fp16 weights or raw codes (device).
  * Passage: the custom dequantization kernels of Section 2.4.
  *   packed   device blob written by qx_pack_layout (copied to the GPU).
  *   out_kind QX_OUT_F16: out = fp16 W' [n][k], uniform W' = fp16_RNE(s*(q-z))
- *            (the exact product, rounded once), codebook W' = C[q].
+ *            (the exact product, rounded once), codebook W' = C[q], Q4X
+ *            W' = fp16_RNE(s*CB[t][q]).
  *            QX_OUT_CODES: out = uint8 codes [n][k].
  *   out      device buffer of n*k*2 (F16) or n*k (CODES) bytes.
  * Results are bit-exact with the definitions above.
@@ -130,6 +164,7 @@ int qx_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y
  *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte
  *   alignment suffices for Y). fp16 matrix-core products, fp32 accumulate,
  *   RNE to fp16. m = 0 or n = 0 is a no-op; m must be <= 65536.
+ *   QX_Q4X matrices are not supported here (QX_E_UNSUPPORTED).
  */
 int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
             hipStream_t stream);

@@ -8,6 +8,7 @@ call raises -- there is no fallback.
 
 Functions keep the C names:
   qx_pack_layout(desc, codes, scales=None, zeros=None, codebook=None) -> uint8 numpy blob
+  qx_pack_q4x(desc, codes, scales, selectors, codebook) -> uint8 numpy blob
   qx_dequant(desc, packed, out_kind, out, stream=None)
   qx_gemv(desc, packed, x, y, stream=None)
   qx_gemm(desc, packed, m, X, Y, stream=None)
@@ -25,7 +26,7 @@ import numpy as np
 
 from . import _build
 
-QX_UNIFORM, QX_CODEBOOK = 0, 1
+QX_UNIFORM, QX_CODEBOOK, QX_Q4X = 0, 1, 2
 QX_OUT_F16, QX_OUT_CODES = 0, 1
 QX_OK, QX_E_ARG, QX_E_UNSUPPORTED, QX_E_SIZE, QX_E_HIP = 0, -1, -2, -3, -4
 
@@ -72,6 +73,8 @@ def load():
         D = ctypes.POINTER(QxDesc)
         L.qx_pack_layout.argtypes = [D, P, P, P, P, P, sz, ctypes.POINTER(sz)]
         L.qx_pack_layout.restype = ctypes.c_int
+        L.qx_pack_q4x.argtypes = [D, P, P, P, P, P, sz, ctypes.POINTER(sz)]
+        L.qx_pack_q4x.restype = ctypes.c_int
         L.qx_dequant.argtypes = [D, P, ctypes.c_int, P, P]
         L.qx_dequant.restype = ctypes.c_int
         L.qx_gemv.argtypes = [D, P, P, P, P]
@@ -121,6 +124,25 @@ def qx_pack_layout(d: QxDesc, codes: np.ndarray, scales=None, zeros=None, codebo
     return out[:size.value]
 
 
+def qx_pack_q4x(d: QxDesc, codes: np.ndarray, scales, selectors, codebook,
+                out: Optional[np.ndarray] = None) -> np.ndarray:
+    """Q4X blob (host uint8 array): codes [n][k], scales [n][k/64] (binary16 bits),
+    selectors [n][k/64] (< 4), codebook [4][16] (binary16 bits)."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    selectors = np.ascontiguousarray(selectors, dtype=np.uint8)
+    codebook = np.ascontiguousarray(codebook, dtype=np.uint16)
+    size = ctypes.c_size_t(0)
+    L = load()
+    _check(L.qx_pack_q4x(ctypes.byref(d), None, None, None, None, None, 0, ctypes.byref(size)),
+           "qx_pack_q4x")
+    if out is None:
+        out = np.empty(size.value, np.uint8)
+    _check(L.qx_pack_q4x(ctypes.byref(d), _np_ptr(codes), _np_ptr(scales), _np_ptr(selectors),
+                         _np_ptr(codebook), _np_ptr(out), out.nbytes, ctypes.byref(size)), "qx_pack_q4x")
+    return out[:size.value]
+
+
 def _dev_ptr(t):
     if t is None:
         return None
@@ -162,8 +184,11 @@ class PackedWeight:
 
     @classmethod
     def from_quant(cls, q, device="cuda") -> "PackedWeight":
-        """From an object with n, k, bits, group, kind, codes, scales, zeros, codebook."""
+        """From an object with n, k, bits, group, kind, codes, scales, zeros, codebook
+        (and selectors for Q4X)."""
         d = desc(q.n, q.k, q.bits, q.group, q.kind)
+        if q.kind == QX_Q4X:
+            return cls(d, qx_pack_q4x(d, q.codes, q.scales, q.selectors, q.codebook), device)
         return cls(d, qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook), device)
 
     def dequant(self, out_kind: int = QX_OUT_F16, stream=None):

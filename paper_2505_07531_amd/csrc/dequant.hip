@@ -1,7 +1,9 @@
 // Dequantization kernel: packed blob -> raw codes (uint8 [n][k]) or fp16 W'
 // [n][k], bit-exact with the definitions (uniform W' = fp16_RNE(s*(q-z)): the
 // exact integers q - z times s in one IEEE fp16 multiply; codebook W' = C[q], a
-// byte copy through the v_perm tables). One lane per (row, 128-code chunk).
+// byte copy through the v_perm tables; Q4X W' = fp16_RNE(s*CB[sel][q]), the
+// table entry times s in one IEEE fp16 multiply). One lane per (row, 128-code
+// chunk).
 #include "qx_device.h"
 #include "qx_internal.h"
 
@@ -57,6 +59,28 @@ __global__ __launch_bounds__(256) void dequant_kernel(const char* __restrict__ p
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[i] = u32x4{q[4 * i], q[4 * i + 1], q[4 * i + 2], q[4 * i + 3]};
     return;
+  } else if constexpr (KIND == QX_Q4X) {
+    // groups 2c (codes 0-63) and 2c + 1 (64-127): the selected sub-codebook's entry
+    // times the group's scale, one IEEE fp16 multiply of the two binary16 values
+    const Q4xOffsets L = q4x_offsets(n, k);
+    const uint32_t sw = *reinterpret_cast<const uint32_t*>(packed + L.scales + ((size_t)row * L.groups + 2 * c) * 2);
+    const uint32_t selw = *reinterpret_cast<const uint32_t*>(packed + L.selectors + ((size_t)row * L.words + c / 8) * 4);
+    const uint32_t* cb = reinterpret_cast<const uint32_t*>(packed + L.codebook);
+    uint32_t w[64];  // fp16 pairs, natural order
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const uint32_t* tab = cb + 8 * ((selw >> (4 * (c % 8) + 2 * g)) & 3u);
+      const uint32_t sp = ((sw >> (16 * g)) & 0xFFFFu) * 0x00010001u;  // (s, s)
+#pragma unroll
+      for (int t = 16 * g; t < 16 * g + 16; ++t) {
+        block_weights<4, QX_CODEBOOK>(q[t], tab, w[2 * t], w[2 * t + 1]);
+        w[2 * t] = hmul2(w[2 * t], sp);
+        w[2 * t + 1] = hmul2(w[2 * t + 1], sp);
+      }
+    }
+    u32x4* o = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + e0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[i] = u32x4{w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
   } else {
     const size_t meta_off = (size_t)n * k * BITS / 8;
     const size_t g0 = (size_t)row * (k / G) + (size_t)c * (128 / G);
@@ -92,6 +116,7 @@ int launch_dequant(const qx_desc* d, const void* packed, int out_kind, void* out
   QX_DQ_CASE(3, 1, 32) QX_DQ_CASE(3, 1, 64) QX_DQ_CASE(3, 1, 128)
   QX_DQ_CASE(4, 0, 32) QX_DQ_CASE(4, 0, 64) QX_DQ_CASE(4, 0, 128)
   QX_DQ_CASE(4, 1, 32) QX_DQ_CASE(4, 1, 64) QX_DQ_CASE(4, 1, 128)
+  QX_DQ_CASE(4, 2, 64)
 #undef QX_DQ_CASE
   return QX_E_UNSUPPORTED;
 }

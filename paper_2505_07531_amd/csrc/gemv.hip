@@ -118,7 +118,8 @@ __device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs,
 template <int BITS, int KIND, int G>
 struct Item {
   static constexpr int kGroups = 128 / G;
-  static constexpr int kMetaDw = KIND == 0 ? kGroups : kGroups * (1 << BITS) / 2;
+  // Q4X: m[0] = the two groups' binary16 scales, m[1] = their selectors (bits 0-1, 2-3)
+  static constexpr int kMetaDw = KIND == QX_Q4X ? 2 : KIND == 0 ? kGroups : kGroups * (1 << BITS) / 2;
   uint32_t d[4 * BITS];
   uint32_t m[kMetaDw];
 };
@@ -131,6 +132,16 @@ __device__ __forceinline__ void load_item(Item<BITS, KIND, G>& it, const char* _
   for (int s = 0; s < BITS; ++s) {
     const u32x4 v = __builtin_nontemporal_load(code + (size_t)s * C);
     it.d[4 * s + 0] = v.x; it.d[4 * s + 1] = v.y; it.d[4 * s + 2] = v.z; it.d[4 * s + 3] = v.w;
+  }
+  if constexpr (KIND == QX_Q4X) {  // groups 2c and 2c + 1 of the row
+    const size_t sel_off = meta_off + meta_off / 16;  // after n*G binary16 scales (n*k/32 bytes)
+    const int W = (G_row + 15) / 16;
+    it.m[0] = __builtin_nontemporal_load(
+        reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + 2 * c) * 2));
+    const uint32_t sw = __builtin_nontemporal_load(
+        reinterpret_cast<const uint32_t*>(packed + sel_off + ((size_t)row * W + c / 8) * 4));
+    it.m[1] = (sw >> (4 * (c % 8))) & 0xFu;
+    return;
   }
   constexpr int kDw = Item<BITS, KIND, G>::kMetaDw;
   const size_t gidx = (size_t)row * G_row + (size_t)c * (128 / G);
@@ -174,10 +185,36 @@ __device__ __forceinline__ float fold_group(uint32_t word, float acc, float2 gsu
 // chunk's (sum M x, sum x) per group and fold_group takes the zero point out.
 template <int BITS, int KIND, int G>
 __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const char* xb,
-                                           const float2* gs, const DecodeConsts& k) {
+                                           const float2* gs, const DecodeConsts& k,
+                                           const uint32_t* q4lut = nullptr) {
   constexpr int NG = 128 / G;
   const u32x4* xv = reinterpret_cast<const u32x4*>(xb);
-  if constexpr (BITS == 4 && KIND == 0) {
+  if constexpr (KIND == QX_Q4X) {
+    // two groups of 64: the selected sub-codebook (lookup tables in LDS), the scale
+    // applied once to each group's sum of table entries times x
+    float part = 0.f;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const uint32_t* tp = q4lut + 8 * ((it.m[1] >> (2 * g)) & 3u);
+      const u32x4 tl = *reinterpret_cast<const u32x4*>(tp), th = *reinterpret_cast<const u32x4*>(tp + 4);
+      const LutGroup<4> t = {{tl.x, tl.y, tl.z, tl.w}, {th.x, th.y, th.z, th.w}};
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 8 * g; j < 8 * g + 8; ++j) {
+        const u32x4 x = xv[j];
+        const uint32_t D = it.d[j];
+        uint32_t elo, ehi, olo, ohi;
+        lut4_bytes(t, D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
+        lut4_bytes(t, (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
+        acc = dot2(perm(ehi, elo, 0x06020400u), x.x, acc);  // (0, 4)
+        acc = dot2(perm(ohi, olo, 0x06020400u), x.y, acc);  // (1, 5)
+        acc = dot2(perm(ehi, elo, 0x07030501u), x.z, acc);  // (2, 6)
+        acc = dot2(perm(ohi, olo, 0x07030501u), x.w, acc);  // (3, 7)
+      }
+      part += half_bits_to_float((it.m[0] >> (16 * g)) & 0xFFFFu) * acc;
+    }
+    return part;
+  } else if constexpr (BITS == 4 && KIND == 0) {
     float part = 0.f;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -296,6 +333,20 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
   }
 }
 
+// Q4X: the matrix's 4 x 16 binary16 codebook as the v_perm lookup tables of
+// lut4_bytes (per sub-codebook 4 dwords of low bytes, then 4 of high bytes),
+// written to LDS by the first 16 threads of the block.
+__device__ __forceinline__ void stage_q4x_lut(const char* __restrict__ packed, int n, int k,
+                                              uint32_t* lut) {
+  if (threadIdx.x < 16) {
+    const int t = threadIdx.x >> 2, i = threadIdx.x & 3;
+    const uint32_t* cb = reinterpret_cast<const uint32_t*>(packed + q4x_offsets(n, k).codebook) + 8 * t;
+    const uint32_t w0 = cb[2 * i], w1 = cb[2 * i + 1];
+    lut[8 * t + i] = perm(w1, w0, 0x06040200u);
+    lut[8 * t + 4 + i] = perm(w1, w0, 0x07050301u);
+  }
+}
+
 // K = 128*LPR with LPR in {32, 64}: a row's chunks fill LPR lanes of one wave, so
 // each row is reduced in registers with DPP and stored by one lane; no LDS
 // partials and no second barrier. A block has WPB waves and stages x once for
@@ -308,6 +359,7 @@ __global__ __launch_bounds__(64 * WPB) void gemv_wave_kernel(const char* __restr
   constexpr int XP = (C * 16 + NT - 1) / NT;
   __shared__ __align__(16) char xs[C * kXBlock];
   __shared__ float2 gs[KIND == QX_UNIFORM ? C * (128 / G) : 1];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const int k = C * 128;
   const size_t meta_off = (size_t)n * k * BITS / 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -319,9 +371,10 @@ __global__ __launch_bounds__(64 * WPB) void gemv_wave_kernel(const char* __restr
   load_x<XP>(x, 0, C, xr, NT);
   Item<BITS, KIND, G> it;
   load_item<BITS, KIND, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);
   store_x<BITS, KIND, G, XP, C * 16 % NT == 0>(xr, C, xs, gs, NT);
   __syncthreads();
-  float v = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc);
+  float v = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc, q4lut);
   v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
   if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v);
 }
@@ -412,6 +465,7 @@ __global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__
   char* xs = smem;                                             // C * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + C * kXBlock);  // R * C floats
   float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(C, R * C));  // C * 128/G
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const DecodeConsts kc = decode_consts();
 
   u32x4 xr[XP];
@@ -422,9 +476,10 @@ __global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__
   const bool valid = r < rows;
   Item<BITS, KIND, G> it;
   load_item<BITS, KIND, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);
   store_x<BITS, KIND, G, XP>(xr, C, xs, gs, nthreads);
   __syncthreads();
-  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc);
+  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, gs + c * (128 / G), kc, q4lut);
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int rr = wave; rr < rows; rr += nthreads >> 6) {
@@ -454,7 +509,9 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
   char* xs = smem;                                              // CT * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + CT * kXBlock);  // R * CT floats
   float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(CT, R * CT));  // CT * 128/G
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const DecodeConsts kc = decode_consts();
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);  // before the first barrier
 
   float acc[ITEMS];
 #pragma unroll
@@ -482,7 +539,7 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j)
-      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock, gs + cl[j] * (128 / G), kc);
+      if (valid[j]) acc[j] += chunk_dot<BITS, KIND, G>(it[j], xs + cl[j] * kXBlock, gs + cl[j] * (128 / G), kc, q4lut);
   }
 
 #pragma unroll
@@ -621,6 +678,7 @@ int launch_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_
   QX_GEMV_CASE(3, 1, 32) QX_GEMV_CASE(3, 1, 64) QX_GEMV_CASE(3, 1, 128)
   QX_GEMV_CASE(4, 0, 32) QX_GEMV_CASE(4, 0, 64) QX_GEMV_CASE(4, 0, 128)
   QX_GEMV_CASE(4, 1, 32) QX_GEMV_CASE(4, 1, 64) QX_GEMV_CASE(4, 1, 128)
+  QX_GEMV_CASE(4, 2, 64)
 #undef QX_GEMV_CASE
   return QX_E_UNSUPPORTED;
 }

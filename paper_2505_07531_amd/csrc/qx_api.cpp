@@ -15,7 +15,8 @@ constexpr int kMaxK = 1 << 20;
 int check_desc(const qx_desc* d) {
   if (d == nullptr) return QX_E_ARG;
   if (d->flags != 0 || d->n < 0 || d->k <= 0 || d->k % 128 != 0 || d->k > kMaxK) return QX_E_ARG;
-  if (d->kind != QX_UNIFORM && d->kind != QX_CODEBOOK) return QX_E_ARG;
+  if (d->kind != QX_UNIFORM && d->kind != QX_CODEBOOK && d->kind != QX_Q4X) return QX_E_ARG;
+  if (d->kind == QX_Q4X && (d->bits != 4 || d->group != 64)) return QX_E_ARG;  // fixed by the format
   if (d->bits < 1 || d->bits > 8 || d->group <= 0 || d->k % d->group != 0) return QX_E_ARG;
   if (d->bits != 3 && d->bits != 4) return QX_E_UNSUPPORTED;
   if (d->group != 32 && d->group != 64 && d->group != 128) return QX_E_UNSUPPORTED;
@@ -30,6 +31,7 @@ size_t meta_bytes_per_group(const qx_desc* d) {
 }
 
 size_t packed_bytes(const qx_desc* d) {
+  if (d->kind == QX_Q4X) return qx::q4x_offsets(d->n, d->k).total;
   const size_t n = (size_t)d->n, k = (size_t)d->k;
   return n * k * d->bits / 8 + n * (k / d->group) * meta_bytes_per_group(d);
 }
@@ -88,7 +90,7 @@ int qx_pack_layout(const qx_desc* d, const uint8_t* codes, const uint16_t* scale
                    size_t* packed_size) {
   const int st = check_desc(d);
   if (st != QX_OK) return st;
-  if (packed_size == nullptr) return QX_E_ARG;
+  if (packed_size == nullptr || d->kind == QX_Q4X) return QX_E_ARG;
   const size_t total = packed_bytes(d);
   *packed_size = total;
   if (packed == nullptr) return QX_OK;
@@ -142,6 +144,42 @@ int qx_pack_layout(const qx_desc* d, const uint8_t* codes, const uint16_t* scale
   return QX_OK;
 }
 
+int qx_pack_q4x(const qx_desc* d, const uint8_t* codes, const uint16_t* scales,
+                const uint8_t* selectors, const uint16_t* codebook, void* packed, size_t cap,
+                size_t* packed_size) {
+  const int st = check_desc(d);
+  if (st != QX_OK) return st;
+  if (packed_size == nullptr || d->kind != QX_Q4X) return QX_E_ARG;
+  const qx::Q4xOffsets L = qx::q4x_offsets(d->n, d->k);
+  *packed_size = L.total;
+  if (packed == nullptr) return QX_OK;
+  if (cap < L.total) return QX_E_SIZE;
+  const size_t n = (size_t)d->n, k = (size_t)d->k, G = (size_t)L.groups;
+  if (codebook == nullptr) return QX_E_ARG;
+  if (n > 0 && (codes == nullptr || scales == nullptr || selectors == nullptr)) return QX_E_ARG;
+  for (size_t i = 0; i < n * k; ++i)
+    if (codes[i] > 15) return QX_E_ARG;
+  for (size_t i = 0; i < n * G; ++i)
+    if (selectors[i] > 3) return QX_E_ARG;
+  uint8_t* blob = static_cast<uint8_t*>(packed);
+  std::memset(blob, 0, L.total);
+  pack_rows(d, codes, 0, d->n, blob);
+  for (size_t i = 0; i < n * G; ++i) {
+    blob[L.scales + 2 * i] = (uint8_t)scales[i];
+    blob[L.scales + 2 * i + 1] = (uint8_t)(scales[i] >> 8);
+  }
+  for (size_t r = 0; r < n; ++r)
+    for (size_t j = 0; j < G; ++j) {
+      const size_t byte = L.selectors + (r * L.words + j / 16) * 4 + (j % 16) / 4;
+      blob[byte] |= (uint8_t)(selectors[r * G + j] << (2 * (j % 4)));
+    }
+  for (int e = 0; e < 64; ++e) {
+    blob[L.codebook + 2 * e] = (uint8_t)codebook[e];
+    blob[L.codebook + 2 * e + 1] = (uint8_t)(codebook[e] >> 8);
+  }
+  return QX_OK;
+}
+
 int qx_dequant(const qx_desc* d, const void* packed, int out_kind, void* out, hipStream_t stream) {
   const int st = check_desc(d);
   if (st != QX_OK) return st;
@@ -166,6 +204,7 @@ int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, 
   const int st = check_desc(d);
   if (st != QX_OK) return st;
   if (m < 0 || m > 65536) return QX_E_ARG;
+  if (d->kind == QX_Q4X) return QX_E_UNSUPPORTED;
   if (m == 0 || d->n == 0) return QX_OK;
   if (packed == nullptr || X == nullptr || Y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(X) || !aligned2(Y)) return QX_E_ARG;

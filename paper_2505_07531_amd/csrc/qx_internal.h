@@ -9,6 +9,24 @@
 
 namespace qx {
 
+// Byte offsets of the Q4X regions after the 4-bit codes of an n x k matrix:
+// binary16 scales per group of 64, ceil(G/16) uint32 selector words per row
+// (2 bits per group), and the 64-entry binary16 codebook at a multiple of 16.
+struct Q4xOffsets {
+  size_t scales, selectors, codebook, total;
+  int groups, words;
+};
+__host__ __device__ inline Q4xOffsets q4x_offsets(int n, int k) {
+  Q4xOffsets o;
+  o.groups = k / 64;
+  o.words = (o.groups + 15) / 16;
+  o.scales = (size_t)n * k / 2;
+  o.selectors = o.scales + (size_t)n * o.groups * 2;
+  o.codebook = (o.selectors + (size_t)n * o.words * 4 + 15) / 16 * 16;
+  o.total = o.codebook + 128;
+  return o;
+}
+
 int launch_dequant(const qx_desc* d, const void* packed, int out_kind, void* out, hipStream_t s);
 int launch_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
                 hipStream_t s);

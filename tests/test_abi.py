@@ -170,3 +170,63 @@ def test_status_strings():
     assert qx.qx_status_str(0) == "ok"
     assert qx.qx_status_str(-3) == "output buffer too small"
     assert qx.qx_status_str(99) == "unknown status"
+
+
+# ------------------------------------------------------------------ Q4X (host side)
+def _random_q4x(n, k, seed):
+    rng = np.random.default_rng(seed)
+    G = k // 64
+    return (rng.integers(0, 16, (n, k), dtype=np.uint8), rng.integers(0, 2**16, (n, G), dtype=np.uint16),
+            rng.integers(0, 4, (n, G), dtype=np.uint8), rng.integers(0, 2**16, (4, 16), dtype=np.uint16))
+
+
+@pytest.mark.parametrize("n,k", [(1, 128), (3, 1152), (5, 11008), (17, 4096), (2, 16384)])
+def test_pack_q4x_matches_oracle_bytes(n, k):
+    codes, s, sel, cb = _random_q4x(n, k, n * 31 + k)
+    blob = qx.qx_pack_q4x(qx.desc(n, k, 4, 64, qx.QX_Q4X), codes, s, sel, cb)
+    assert np.array_equal(blob, oracle.q4x.pack(codes, s, sel, cb))
+
+
+def test_pack_q4x_quantized_matrix_matches_oracle_bytes():
+    from qx_inputs import q4x as qq
+    q = qq.quantize_q4x(qi.weights("t4", 0.0141421, 4, 3, 40, 1152))
+    blob = qx.qx_pack_q4x(qx.desc(40, 1152, 4, 64, qx.QX_Q4X), q.codes, q.scales, q.selectors, q.codebook)
+    assert np.array_equal(blob, oracle.q4x.pack(q.codes, q.scales, q.selectors, q.codebook))
+
+
+def test_pack_q4x_errors_and_capacity():
+    n, k = 2, 256
+    codes, s, sel, cb = _random_q4x(n, k, 1)
+    d = qx.desc(n, k, 4, 64, qx.QX_Q4X)
+    ok = lambda dd=d, **kw: _st(lambda: qx.qx_pack_q4x(dd, **{**dict(codes=codes, scales=s, selectors=sel,
+                                                                      codebook=cb), **kw}))
+    assert ok() == qx.QX_OK
+    assert ok(codes=np.full((n, k), 16, np.uint8)) == qx.QX_E_ARG
+    assert ok(selectors=np.full((n, 4), 4, np.uint8)) == qx.QX_E_ARG
+    assert ok(dd=qx.desc(n, k, 3, 64, qx.QX_Q4X)) == qx.QX_E_ARG    # the format fixes b = 4
+    assert ok(dd=qx.desc(n, k, 4, 128, qx.QX_Q4X)) == qx.QX_E_ARG   # and g = 64
+    assert ok(dd=qx.desc(n, k, 4, 64, qx.QX_CODEBOOK)) == qx.QX_E_ARG
+    size = oracle.q4x.packed_size(n, k)
+    small = np.empty(size - 1, np.uint8)
+    assert ok(out=small) == qx.QX_E_SIZE
+    # the general packer does not take Q4X descriptors
+    assert _st(lambda: qx.qx_pack_layout(d, codes)) == qx.QX_E_ARG
+    lib = qx.load()
+    sz = ctypes.c_size_t(0)
+    P = ctypes.c_void_p
+    assert lib.qx_pack_q4x(ctypes.byref(d), None, None, None, None, None, 0, ctypes.byref(sz)) == qx.QX_OK
+    assert sz.value == size
+    out = np.empty(size, np.uint8)
+    assert lib.qx_pack_q4x(ctypes.byref(d), codes.ctypes.data_as(P), None, sel.ctypes.data_as(P),
+                           cb.ctypes.data_as(P), out.ctypes.data_as(P), size, ctypes.byref(sz)) == qx.QX_E_ARG
+
+
+def test_q4x_device_calls_reject_before_launch():
+    lib = qx.load()
+    d = qx.desc(4, 128, 4, 64, qx.QX_Q4X)
+    P = ctypes.c_void_p
+    assert lib.qx_gemm(ctypes.byref(d), P(16), 4, P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    assert lib.qx_gemv(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_dequant(ctypes.byref(d), P(8), 0, P(16), None) == qx.QX_E_ARG
+    bad = qx.desc(4, 128, 4, 32, qx.QX_Q4X)
+    assert lib.qx_gemv(ctypes.byref(bad), P(16), P(16), P(16), None) == qx.QX_E_ARG
