@@ -15,7 +15,9 @@ and the CPU oracle timed on a bounded sample.
 
 Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
---workload c5 (prefill GEMM, m = 16, 64, 512), --workload floor (plain read of
+--workload c5 (prefill GEMM, m = 16, 64, 512), --workload q4x (the paper's Q4X
+format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
+rotated over copies like c1-c3), --workload floor (plain read of
 the same byte counts and empty grids: the floor of a one-launch GEMV) and
 --workload counters (the run that the FETCH_SIZE / WRITE_SIZE passes profile).
 """
@@ -296,7 +298,10 @@ def bench_decode(args, qx):
 def rotated_copies(qx, spec, device, min_total=512 << 20):
     q = spec.quantized()
     d = qx.desc(q.n, q.k, q.bits, q.group, q.kind)
-    blob = qx.qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook)
+    if q.kind == qx.QX_Q4X:
+        blob = qx.qx_pack_q4x(d, q.codes, q.scales, q.selectors, q.codebook)
+    else:
+        blob = qx.qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook)
     import torch
     reps = max(2, -(-min_total // blob.size))
     base = torch.from_numpy(blob).to(device)
@@ -308,7 +313,10 @@ def bench_single_gemv(args, qx, name):
     import torch
     from qx_inputs import configs
     dev = torch.device("cuda:0")
-    spec, x = getattr(configs, name)()
+    if name.startswith("q4x."):
+        spec, x = configs.q4x_matrix(name[4:]), configs.q4x_activation(name[4:])
+    else:
+        spec, x = getattr(configs, name)()
     d, copies = rotated_copies(qx, spec, dev)
     xd = torch.from_numpy(x).to(dev)
     y = torch.empty(spec.n, dtype=torch.float16, device=dev)
@@ -325,8 +333,8 @@ def bench_single_gemv(args, qx, name):
             "ms_per_step": round(ms, 6), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "f16", "data": "synthetic",
             "config": {"workload": f"{name}: {spec.n}x{spec.k} {spec.bits}-bit "
-                                   f"{'uniform' if spec.kind == 0 else 'codebook'} g{spec.group}, "
-                                   f"graph of back-to-back launches over {len(copies)} copies",
+                                   f"{['uniform', 'codebook', 'Q4X (4 x 16 matrix codebook, scale + 2-bit selector per group)'][spec.kind]} "
+                                   f"g{spec.group}, graph of back-to-back launches over {len(copies)} copies",
                        "copies": len(copies), "packed_bytes": spec.packed_bytes},
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
@@ -443,7 +451,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "c1", "c2", "c3", "c5", "counters", "floor"])
+                    choices=["decode7b", "c1", "c2", "c3", "c5", "q4x", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -473,6 +481,9 @@ def main():
     elif args.workload == "c5":
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)
+    elif args.workload == "q4x":
+        for name in ("q4x.gate", "q4x.down"):
+            print(json.dumps(bench_single_gemv(args, qx, name)), flush=True)
     else:
         print(json.dumps(bench_single_gemv(args, qx, args.workload)), flush=True)
 

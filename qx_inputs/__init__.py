@@ -205,4 +205,9 @@ def quantize_codebook(w: np.ndarray, bits: int, group: int, max_iter: int = 100,
 
 
 def quantize(w: np.ndarray, bits: int, group: int, kind: int) -> QuantWeight:
+    if kind == Q4X:
+        if bits != 4 or group != 64:
+            raise ValueError("Q4X has 4-bit codes in groups of 64")
+        from .q4x import quantize_q4x
+        return quantize_q4x(w)
     return quantize_uniform(w, bits, group) if kind == UNIFORM else quantize_codebook(w, bits, group)

@@ -15,7 +15,7 @@ from typing import List, Optional
 
 import numpy as np
 
-from . import (CODEBOOK, UNIFORM, QuantWeight, activations, fill, outlier_channels, quantize,
+from . import (CODEBOOK, Q4X, UNIFORM, QuantWeight, activations, fill, outlier_channels, quantize,
                weights)
 
 HIDDEN, MLP, LAYERS = 4096, 11008, 32
@@ -47,8 +47,12 @@ class MatrixSpec:
 
     @property
     def packed_bytes(self) -> int:
-        """Code bytes plus per-group table bytes (the bits-per-weight footprint)."""
+        """Code bytes plus per-group table bytes (the bits-per-weight footprint); for Q4X
+        also the per-row selector words, the alignment padding and the 128-byte codebook."""
         G = self.k // self.group
+        if self.kind == Q4X:
+            sel_words = self.n * ((G + 15) // 16) * 4
+            return (self.n * self.k // 2 + self.n * G * 2 + sel_words + 15) // 16 * 16 + 128
         meta = 4 if self.kind == UNIFORM else 2 * (1 << self.bits)
         return self.n * self.k * self.bits // 8 + self.n * G * meta
 
@@ -117,3 +121,15 @@ def c5_activations(m: int) -> tuple:
     xin = fill("normal", 1.0, 4, 10_000 + m, 0, m * HIDDEN).astype(np.float16).reshape(m, HIDDEN)
     xdn = fill("normal", 1.0, 4, 20_000 + m, 0, m * MLP).astype(np.float16).reshape(m, MLP)
     return xin, xdn
+
+
+def q4x_matrix(name: str) -> MatrixSpec:
+    """The paper's Q4X format (4-bit indices into a per-matrix 4 x 16 codebook, groups of 64)
+    on MLP-shaped weights: gate 11008x4096 and down 4096x11008, Student-t(4) std 0.02."""
+    j = ("gate", "down").index(name)
+    n, k = (MLP, HIDDEN) if name == "gate" else (HIDDEN, MLP)
+    return MatrixSpec(f"q4x.{name}", n, k, "t4", T4_STD, 5, j, 4, 64, Q4X)
+
+
+def q4x_activation(name: str) -> np.ndarray:
+    return activations(5, 100 + ("gate", "down").index(name), HIDDEN if name == "gate" else MLP)
