@@ -22,12 +22,17 @@ its layout and dequantization in ``q4x``:
 
   W'[n,k] = fp16_RNE( s[n,j] * CB[sel[n,j]][q[n,k]] ),  j = k // 64
 
+8-bit activations (Section 2.4; the W3A8 rows of Table 1): ``a8`` quantizes x
+per vector to int8 (symmetric, round to nearest) and multiplies uniform codes
+in exact integer arithmetic.
+
 Modules: ``layout`` (pack/unpack of the packed layout), ``dequant``,
 ``matmul`` (fp64 products and the error metric), ``formats`` (sizes and
-bits-per-weight), ``q4x``.
+bits-per-weight), ``q4x``, ``a8``.
 """
 from .layout import chunk_bit_positions, pack, unpack  # noqa: F401
 from .dequant import dequant, dequant_packed  # noqa: F401
 from .matmul import gemv, gemm, normwise_rel_err  # noqa: F401
 from .formats import packed_size, bits_per_weight  # noqa: F401
 from . import q4x  # noqa: F401
+from . import a8  # noqa: F401

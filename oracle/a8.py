@@ -1,0 +1,50 @@
+"""Oracle of the 8-bit-activation path (test infrastructure).
+
+The paper quantizes activations to 8 bits and not below (Section 2.4), and its
+W3A8G128 configurations (Table 1) and all of Table 2 use 8-bit round-to-nearest
+per-token activations. Per token here means per activation vector: one
+symmetric scale for the whole vector.
+
+  amax  = max_k |x[k]|                 (x binary16, taken exactly in fp32)
+  inv   = fp32(127 / amax),  s_x = fp32(amax / 127)       (amax = 0: xq = 0, s_x = 0)
+  xq[k] = clamp(RNE(fp32(x[k] * inv)), -127, 127)          int8
+  y[n]  = s_x * sum_j s[n,j] * sum_{k in group j} (q[n,k] - z[n,j]) * xq[k]
+
+Every step that decides an integer (the scale and each rounded xq) is taken in
+fp32, the precision the GPU uses for it, so both sides reach the same int8
+codes; the sums are exact integers and the scaling is done in fp64 here. The
+weights enter as the exact s * (q - z) of each uniform level (the integer
+product path never rounds W' to binary16).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def quantize_activation(x16) -> tuple:
+    """(xq int8 [k], s_x float32) of one binary16 activation vector."""
+    x = np.asarray(x16, dtype=np.float16).astype(np.float32)
+    amax = np.float32(np.max(np.abs(x))) if x.size else np.float32(0)
+    if amax == 0:
+        return np.zeros(x.shape, np.int8), np.float32(0)
+    inv = np.float32(np.float32(127.0) / amax)
+    s_x = np.float32(amax / np.float32(127.0))
+    q = np.rint(x * inv)  # fp32 product, then nearest-even
+    return np.clip(q, -127, 127).astype(np.int8), s_x
+
+
+def gemv_a8(codes, group, scales, zeros, x16) -> np.ndarray:
+    """fp64 y [n] of uniform codes [n][k] (binary16 scales/zeros [n][k/g]) and fp16 x [k]."""
+    codes = np.asarray(codes).astype(np.int64)
+    n, k = codes.shape
+    G = k // group
+    xq, s_x = quantize_activation(x16)
+    s = np.asarray(scales, np.uint16).reshape(n, G).view(np.float16).astype(np.float64)
+    z = np.asarray(zeros, np.uint16).reshape(n, G).view(np.float16).astype(np.int64)
+    j = np.arange(k) // group
+    d = codes - z[:, j]                                     # exact integers
+    per_group = np.zeros((n, G), dtype=np.int64)
+    prod = d * xq.astype(np.int64)[None, :]
+    for g in range(G):
+        per_group[:, g] = prod[:, g * group:(g + 1) * group].sum(axis=1)
+    return float(s_x) * (s * per_group.astype(np.float64)).sum(axis=1)

@@ -1,0 +1,69 @@
+"""Pins of the 8-bit-activation oracle (CPU only): per-token symmetric RTN
+(Section 2.4; Table 1's W3A8 configurations) and the integer-domain product of
+uniform codes with int8 activations."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import a8
+import qx_inputs as qi
+
+
+def test_activation_by_hand():
+    x = np.float16([0.5, -1.0, 0.25, 2.0, -2.0, 0.0, 1.0 / 3])
+    xq, s = a8.quantize_activation(x)
+    assert s == np.float32(2.0) / np.float32(127.0)
+    # 0.5 * 63.5 = 31.75 -> 32; -1 -> -63.5 -> -64 (ties to even); 0.25 -> 15.875 -> 16
+    assert xq.tolist() == [32, -64, 16, 127, -127, 0, 21]
+
+
+def test_activation_extremes_and_bound():
+    x = qi.activations(3, 1, 4096, outliers=np.arange(0, 4096, 97))
+    xq, s = a8.quantize_activation(x)
+    xf = x.astype(np.float64)
+    assert np.abs(xq).max() == 127 and xq[np.argmax(np.abs(xf))] in (127, -127)
+    # each code is the nearest integer to x / s_x (up to fp32 rounding of the product)
+    err = np.abs(xf / float(s) - xq.astype(np.float64))
+    assert err.max() <= 0.5 + 1e-5
+    assert np.all(np.abs(xf - float(s) * xq) <= float(s) * (0.5 + 1e-5))
+
+
+def test_zero_activation():
+    xq, s = a8.quantize_activation(np.zeros(256, np.float16))
+    assert s == 0 and not xq.any()
+    q = qi.quantize_uniform(qi.weights("t4", 0.02, 1, 2, 4, 256), 4, 64)
+    assert not a8.gemv_a8(q.codes, 64, q.scales, q.zeros, np.zeros(256, np.float16)).any()
+
+
+@pytest.mark.parametrize("bits,group", [(3, 64), (4, 128), (3, 32)])
+def test_gemv_a8_brute_force(bits, group):
+    rng = np.random.default_rng(bits * group)
+    n, k = 5, 256
+    q = qi.quantize_uniform(qi.weights("t4", 0.02, 2, bits, n, k), bits, group)
+    x = np.float16(rng.standard_normal(k))
+    y = a8.gemv_a8(q.codes, group, q.scales, q.zeros, x)
+    xq, s_x = a8.quantize_activation(x)
+    s = q.scales.view(np.float16).astype(np.float64)
+    z = q.zeros.view(np.float16).astype(np.float64)
+    for r in range(n):
+        tot = 0.0
+        for g in range(k // group):
+            acc = 0
+            for i in range(g * group, (g + 1) * group):
+                acc += (int(q.codes[r, i]) - int(z[r, g])) * int(xq[i])
+            tot += s[r, g] * acc
+        assert y[r] == pytest.approx(float(s_x) * tot, rel=1e-12, abs=1e-12)
+
+
+def test_gemv_a8_close_to_a16():
+    """Quantizing x to 8 bits moves y by at most s_x/2 * sum_k |W'| per row (plus the
+    binary16 rounding of W' that the A16 path applies)."""
+    n, k = 64, 4096
+    q = qi.quantize_uniform(qi.weights("t4", 0.02, 4, 5, n, k), 4, 128)
+    x = qi.activations(4, 6, k)
+    y8 = a8.gemv_a8(q.codes, 128, q.scales, q.zeros, x)
+    w16 = oracle.dequant(q.codes, 128, 0, q.scales, q.zeros).astype(np.float64)
+    y16 = w16 @ x.astype(np.float64)
+    _, s_x = a8.quantize_activation(x)
+    bound = float(s_x) / 2 * np.abs(w16).sum(axis=1) + 2.0**-11 * (np.abs(w16) @ np.abs(x.astype(np.float64)))
+    assert np.all(np.abs(y8 - y16) <= bound * (1 + 1e-9))
