@@ -11,6 +11,7 @@ Functions keep the C names:
   qx_pack_q4x(desc, codes, scales, selectors, codebook) -> uint8 numpy blob
   qx_dequant(desc, packed, out_kind, out, stream=None)
   qx_gemv(desc, packed, x, y, stream=None)
+  qx_gemv_a8(desc, packed, x, y, stream=None)
   qx_gemm(desc, packed, m, X, Y, stream=None)
   qx_status_str(status)
 Tensor arguments are torch CUDA tensors (HIP device memory); ``stream`` is a
@@ -79,6 +80,8 @@ def load():
         L.qx_dequant.restype = ctypes.c_int
         L.qx_gemv.argtypes = [D, P, P, P, P]
         L.qx_gemv.restype = ctypes.c_int
+        L.qx_gemv_a8.argtypes = [D, P, P, P, P]
+        L.qx_gemv_a8.restype = ctypes.c_int
         L.qx_gemm.argtypes = [D, P, ctypes.c_int32, P, P, P]
         L.qx_gemm.restype = ctypes.c_int
         L.qx_status_str.argtypes = [ctypes.c_int]
@@ -167,6 +170,11 @@ def qx_gemv(d: QxDesc, packed, x, y, stream=None) -> None:
                           _stream(stream)), "qx_gemv")
 
 
+def qx_gemv_a8(d: QxDesc, packed, x, y, stream=None) -> None:
+    _check(load().qx_gemv_a8(ctypes.byref(d), _dev_ptr(packed), _dev_ptr(x), _dev_ptr(y),
+                             _stream(stream)), "qx_gemv_a8")
+
+
 def qx_gemm(d: QxDesc, packed, m: int, X, Y, stream=None) -> None:
     _check(load().qx_gemm(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(X), _dev_ptr(Y),
                           _stream(stream)), "qx_gemm")
@@ -203,6 +211,13 @@ class PackedWeight:
         if y is None:
             y = torch.empty(self.desc.n, dtype=torch.float16, device=x.device)
         qx_gemv(self.desc, self.data, x, y, stream)
+        return y
+
+    def gemv_a8(self, x, y=None, stream=None):
+        import torch
+        if y is None:
+            y = torch.empty(self.desc.n, dtype=torch.float16, device=x.device)
+        qx_gemv_a8(self.desc, self.data, x, y, stream)
         return y
 
     def gemm(self, X, Y=None, stream=None):

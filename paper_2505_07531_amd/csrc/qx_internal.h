@@ -32,5 +32,7 @@ int launch_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_
                 hipStream_t s);
 int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y,
                 hipStream_t s);
+int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
+                   hipStream_t s);
 
 }  // namespace qx

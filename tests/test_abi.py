@@ -230,3 +230,18 @@ def test_q4x_device_calls_reject_before_launch():
     assert lib.qx_dequant(ctypes.byref(d), P(8), 0, P(16), None) == qx.QX_E_ARG
     bad = qx.desc(4, 128, 4, 32, qx.QX_Q4X)
     assert lib.qx_gemv(ctypes.byref(bad), P(16), P(16), P(16), None) == qx.QX_E_ARG
+
+
+def test_gemv_a8_rejects_before_launch():
+    lib = qx.load()
+    P = ctypes.c_void_p
+    for kind, bits, group in ((qx.QX_CODEBOOK, 3, 128), (qx.QX_Q4X, 4, 64)):
+        d = qx.desc(4, 128, bits, group, kind)
+        assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    long_k = qx.desc(4, 89 * 128, 4, 128, qx.QX_UNIFORM)
+    assert lib.qx_gemv_a8(ctypes.byref(long_k), P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    d = qx.desc(4, 128, 4, 128, qx.QX_UNIFORM)
+    assert lib.qx_gemv_a8(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(24), P(16), None) == qx.QX_E_ARG
+    z = qx.desc(0, 128, 4, 128, qx.QX_UNIFORM)
+    assert lib.qx_gemv_a8(ctypes.byref(z), None, None, None, None) == qx.QX_OK
