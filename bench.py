@@ -17,7 +17,8 @@ Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
 --workload c5 (prefill GEMM, m = 16, 64, 512), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
-rotated over copies like c1-c3), --workload floor (plain read of
+rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
+matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
 the same byte counts and empty grids: the floor of a one-launch GEMV) and
 --workload counters (the run that the FETCH_SIZE / WRITE_SIZE passes profile).
 """
@@ -309,32 +310,38 @@ def rotated_copies(qx, spec, device, min_total=512 << 20):
     return d, copies
 
 
-def bench_single_gemv(args, qx, name):
+def bench_single_gemv(args, qx, name, a8=False):
     import torch
     from qx_inputs import configs
     dev = torch.device("cuda:0")
     if name.startswith("q4x."):
         spec, x = configs.q4x_matrix(name[4:]), configs.q4x_activation(name[4:])
+    elif name == "gateup":  # the fused gate|up matrix of the decode step, layer 0
+        spec = configs.MatrixSpec("gate|up", 2 * configs.MLP, configs.HIDDEN, "t4", configs.T4_STD,
+                                  3, 900, 4, 128, configs.UNIFORM)
+        x = configs.c4_activation(0, 2)
     else:
         spec, x = getattr(configs, name)()
+    gemv = qx.qx_gemv_a8 if a8 else qx.qx_gemv
     d, copies = rotated_copies(qx, spec, dev)
     xd = torch.from_numpy(x).to(dev)
     y = torch.empty(spec.n, dtype=torch.float16, device=dev)
     def launch_all():
         for c in copies:
-            qx.qx_gemv(d, c, xd, y)
+            gemv(d, c, xd, y)
     reps = max(3, args.steps // len(copies))
     ms = time_graph(launch_all, torch.cuda.Stream(), reps, 2) / len(copies)
     alg = spec.packed_bytes + 2 * (spec.n + spec.k)
     gbs = alg / (ms * 1e-3) / 1e9
     traffic = committed_traffic(f"gemv_{name}")
-    return {"metric": f"batch-1 qGEMV effective HBM GB/s ({name})", "value": round(gbs, 2),
+    act = "int8 activations (per-token RTN, qx_gemv_a8)" if a8 else "fp16 activations"
+    return {"metric": f"batch-1 qGEMV effective HBM GB/s ({name}{', A8' if a8 else ''})", "value": round(gbs, 2),
             "unit": "GB/s", "n_gpus": 1, "steps": reps * len(copies), "warmup": 2 * len(copies),
             "ms_per_step": round(ms, 6), "higher_is_better": True, "scaling": "weak",
-            "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+            "vs_baseline": None, "dtype": "i8" if a8 else "f16", "data": "synthetic",
             "config": {"workload": f"{name}: {spec.n}x{spec.k} {spec.bits}-bit "
                                    f"{['uniform', 'codebook', 'Q4X (4 x 16 matrix codebook, scale + 2-bit selector per group)'][spec.kind]} "
-                                   f"g{spec.group}, graph of back-to-back launches over {len(copies)} copies",
+                                   f"g{spec.group}, {act}, graph of back-to-back launches over {len(copies)} copies",
                        "copies": len(copies), "packed_bytes": spec.packed_bytes},
             "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
@@ -451,7 +458,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "c1", "c2", "c3", "c5", "q4x", "counters", "floor"])
+                    choices=["decode7b", "c1", "c2", "c3", "c5", "q4x", "a8", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -481,6 +488,10 @@ def main():
     elif args.workload == "c5":
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)
+    elif args.workload == "a8":
+        for name in ("c1", "c2", "gateup"):
+            for a8 in (False, True):
+                print(json.dumps(bench_single_gemv(args, qx, name, a8)), flush=True)
     elif args.workload == "q4x":
         for name in ("q4x.gate", "q4x.down"):
             print(json.dumps(bench_single_gemv(args, qx, name)), flush=True)

@@ -5,16 +5,18 @@ W3A8G128 configurations (Table 1) and all of Table 2 use 8-bit round-to-nearest
 per-token activations. Per token here means per activation vector: one
 symmetric scale for the whole vector.
 
-  amax  = max_k |x[k]|                 (x binary16, taken exactly in fp32)
+  amax  = max_k |x[k]|                 (x binary16, exact)
   inv   = fp32(127 / amax),  s_x = fp32(amax / 127)       (amax = 0: xq = 0, s_x = 0)
-  xq[k] = clamp(RNE(fp32(x[k] * inv)), -127, 127)          int8
+  xq[k] = clamp(RNE(x[k] * inv), -127, 127)                int8, the product exact
   y[n]  = s_x * sum_j s[n,j] * sum_{k in group j} (q[n,k] - z[n,j]) * xq[k]
 
-Every step that decides an integer (the scale and each rounded xq) is taken in
-fp32, the precision the GPU uses for it, so both sides reach the same int8
-codes; the sums are exact integers and the scaling is done in fp64 here. The
-weights enter as the exact s * (q - z) of each uniform level (the integer
-product path never rounds W' to binary16).
+The steps that decide an integer are the ones the GPU takes: the fp32 scale
+inv, and the nearest integer to the exact product of a binary16 x and the fp32
+inv (at most 35 significant bits, exact in fp64 here; one fused multiply-add
+with a rounding constant there), so both sides reach the same int8 codes; the
+sums are exact integers and the scaling is done in fp64 here. The weights
+enter as the exact s * (q - z) of each uniform level (the integer product path
+never rounds W' to binary16).
 """
 from __future__ import annotations
 
@@ -29,7 +31,7 @@ def quantize_activation(x16) -> tuple:
         return np.zeros(x.shape, np.int8), np.float32(0)
     inv = np.float32(np.float32(127.0) / amax)
     s_x = np.float32(amax / np.float32(127.0))
-    q = np.rint(x * inv)  # fp32 product, then nearest-even
+    q = np.rint(x.astype(np.float64) * np.float64(inv))  # exact product, then nearest-even
     return np.clip(q, -127, 127).astype(np.int8), s_x
 
 

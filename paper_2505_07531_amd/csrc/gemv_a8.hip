@@ -2,8 +2,8 @@
 // and not below (Section 2.4), and its W3A8 configurations (Table 1) and Table
 // 2's runs quantize them per token by round-to-nearest. Here one activation
 // vector gets one symmetric scale,
-//   amax = max |x|, inv = 127 / amax, xq = clamp(rint(x * inv), -127, 127),
-//   s_x = amax / 127   (fp32; amax = 0 gives xq = 0 and y = 0),
+//   amax = max |x|, inv = 127 / amax (fp32), xq = nearest integer to x * inv
+//   (the product exact), s_x = amax / 127 (fp32; amax = 0 gives xq = 0, y = 0),
 // and uniform codes are multiplied with xq in exact integers:
 //   y[n] = s_x * sum_j s_j * (sum_{k in j} q*xq - z_j * sum_{k in j} xq).
 //
@@ -57,12 +57,16 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-__device__ __forceinline__ int q8(float v, float inv) {
-  return (int)fminf(fmaxf(__builtin_rintf(v * inv), -127.f), 127.f);
+// x * inv + 1.5 * 2^23 in one fused multiply-add (the fp16 x widened exactly): the
+// sum lies in [2^23, 2^24), where fp32 steps by 1, so its single rounding is the
+// nearest-even integer to the exact product, and the low byte of the result's bits
+// is that integer as int8 (|x * inv| <= 127 since |x| <= amax).
+__device__ __forceinline__ uint32_t q8_bits(_Float16 v, float inv) {
+  return __builtin_bit_cast(uint32_t, __builtin_fmaf((float)v, inv, 12582912.0f));
 }
-__device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
-  return (uint32_t)(a & 0xFF) | ((uint32_t)(b & 0xFF) << 8) | ((uint32_t)(c & 0xFF) << 16) |
-         ((uint32_t)(d & 0xFF) << 24);
+// int8 bytes of four q8_bits values, in argument order
+__device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return perm(perm(d, c, 0x04000C0Cu), perm(b, a, 0x0C0C0400u), 0x07060100u);
 }
 
 // Quantize the staged pieces of x (XP 16-byte pieces per thread, piece p = chunk
@@ -73,14 +77,15 @@ __device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
 template <int BITS, int G, int XP>
 __device__ __forceinline__ float stage_x_a8(const u32x4 (&xr)[XP], int C, char* xs, float* gs,
                                             float* red, int nthreads) {
-  float m = 0.f;
+  h2_t mh = {(_Float16)0, (_Float16)0};
 #pragma unroll
   for (int i = 0; i < XP; ++i) {  // clamped duplicates of valid pieces leave the max unchanged
     const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
 #pragma unroll
     for (int t = 0; t < 4; ++t)
-      m = fmaxf(m, fmaxf(fabsf(half_bits_to_float(w[t] & 0xFFFFu)), fabsf(half_bits_to_float(w[t] >> 16))));
+      mh = __builtin_elementwise_max(mh, __builtin_elementwise_abs(__builtin_bit_cast(h2_t, w[t])));
   }
+  float m = fmaxf((float)mh.x, (float)mh.y);
   m = wave_max(m);
   const int wave = threadIdx.x >> 6, nwaves = nthreads >> 6;
   if ((threadIdx.x & 63) == 0) red[wave] = m;
@@ -92,26 +97,25 @@ __device__ __forceinline__ float stage_x_a8(const u32x4 (&xr)[XP], int C, char* 
   for (int i = 0; i < XP; ++i) {
     const int p = threadIdx.x + i * nthreads;
     const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
-    int q[8];
+    uint32_t q[8];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      q[2 * t] = q8(half_bits_to_float(w[t] & 0xFFFFu), inv);
-      q[2 * t + 1] = q8(half_bits_to_float(w[t] >> 16), inv);
+      const h2_t h = __builtin_bit_cast(h2_t, w[t]);
+      q[2 * t] = q8_bits(h.x, inv);
+      q[2 * t + 1] = q8_bits(h.y, inv);
+    }
+    u32x2 o;
+    if constexpr (BITS == 4) {
+      o.x = pack4(q[0], q[2], q[4], q[6]);
+      o.y = pack4(q[1], q[3], q[5], q[7]);
+    } else {
+      o.x = pack4(q[0], q[1], q[2], q[3]);
+      o.y = pack4(q[4], q[5], q[6], q[7]);
     }
     const bool valid = p < C * 16;
-    if (valid) {
-      u32x2 o;
-      if constexpr (BITS == 4) {
-        o.x = pack4(q[0], q[2], q[4], q[6]);
-        o.y = pack4(q[1], q[3], q[5], q[7]);
-      } else {
-        o.x = pack4(q[0], q[1], q[2], q[3]);
-        o.y = pack4(q[4], q[5], q[6], q[7]);
-      }
-      *reinterpret_cast<u32x2*>(xs + (p >> 4) * kX8Block + (p & 15) * 8) = o;
-    }
+    if (valid) *reinterpret_cast<u32x2*>(xs + (p >> 4) * kX8Block + (p & 15) * 8) = o;
     constexpr int PPG = G / 8;  // pieces per group, consecutive lanes
-    float s = (float)(q[0] + q[1] + q[2] + q[3] + q[4] + q[5] + q[6] + q[7]);
+    float s = (float)__builtin_amdgcn_sdot4((int)o.y, 0x01010101, __builtin_amdgcn_sdot4((int)o.x, 0x01010101, 0, false), false);
     if constexpr (PPG >= 4) {
       s = dpp_plus<0xB1, 0xF>(s);
       s = dpp_plus<0x4E, 0xF>(s);

@@ -22,7 +22,10 @@ def test_activation_extremes_and_bound():
     xq, s = a8.quantize_activation(x)
     xf = x.astype(np.float64)
     assert np.abs(xq).max() == 127 and xq[np.argmax(np.abs(xf))] in (127, -127)
-    # each code is the nearest integer to x / s_x (up to fp32 rounding of the product)
+    # each code is the nearest integer to x * inv (exact product), so within 1/2 of x / s_x
+    # up to the relative rounding of inv and s_x
+    _, inv = 0, np.float32(127.0) / np.float32(np.abs(xf).max())
+    assert np.all(np.abs(xf * np.float64(inv) - xq) <= 0.5)
     err = np.abs(xf / float(s) - xq.astype(np.float64))
     assert err.max() <= 0.5 + 1e-5
     assert np.all(np.abs(xf - float(s) * xq) <= float(s) * (0.5 + 1e-5))
