@@ -15,7 +15,8 @@ and the CPU oracle timed on a bounded sample.
 
 Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
---workload c5 (prefill GEMM, m = 16, 64, 512), --workload q4x (the paper's Q4X
+--workload batch (the same decode step for 1 to 4 sequences decoded together,
+one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
 rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
 matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
@@ -39,7 +40,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, published
 FP16_MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 matrix-core peak, published
 METRIC = "batch-1 qGEMV effective HBM GB/s (% of peak) + µs per 7B decode step"
-KERNEL_SOURCES = ["qx_device.h", "gemv.hip", "gemm.hip", "dequant.hip"]
+KERNEL_SOURCES = ["qx_device.h", "gemv_common.h", "gemv.hip", "gemm.hip", "dequant.hip"]
 
 
 def log(msg: str) -> None:
@@ -92,7 +93,7 @@ class DecodeStep:
     launches (qkv, o, gate|up, down) and the outputs are the same rows.
     """
 
-    def __init__(self, qx, device, plan, quant, fused=False):
+    def __init__(self, qx, device, plan, quant, fused=False, batch=1):
         import torch
         from qx_inputs import configs
         self.plan = plan
@@ -114,28 +115,33 @@ class DecodeStep:
             for i, q in enumerate(quant):
                 self.launches.append((qx.PackedWeight.from_quant(q, device=device),
                                       self.plan[i][1], [(0, i)]))
+        self.batch = batch
         self.x = {}
         for l in range(layers):
             for t in range(4):
-                self.x[(l, t)] = torch.from_numpy(configs.c4_activation(l, t)).to(device)
-        self.y = [torch.empty(pw.desc.n, dtype=torch.float16, device=device)
-                  for pw, _, _ in self.launches]
+                xv = configs.c4_activation(l, t) if batch == 1 else configs.c4_batch_activations(l, t, batch)
+                self.x[(l, t)] = torch.from_numpy(xv).to(device)
+        self.y = [torch.empty((batch, pw.desc.n) if batch > 1 else pw.desc.n, dtype=torch.float16,
+                              device=device) for pw, _, _ in self.launches]
         self.packed_bytes = sum(spec.packed_bytes for spec, _ in self.plan)
         self.act_bytes = sum(2 * (spec.n + spec.k) for spec, _ in self.plan)
         self.qx = qx
 
     def output(self, plan_index):
-        """Device view of the y of GEMV `plan_index` of the plan."""
+        """Device view of the y of GEMV `plan_index` of the plan ([batch][n] when batch > 1)."""
         for (pw, _, offs), y in zip(self.launches, self.y):
             for off, i in offs:
                 if i == plan_index:
-                    return y[off:off + self.plan[i][0].n]
+                    return y[..., off:off + self.plan[i][0].n]
         raise KeyError(plan_index)
 
     def launch(self, stream=None):
         qx = self.qx
         for (pw, xi, _), y in zip(self.launches, self.y):
-            qx.qx_gemv(pw.desc, pw.data, self.x[xi], y, stream)
+            if self.batch == 1:
+                qx.qx_gemv(pw.desc, pw.data, self.x[xi], y, stream)
+            else:
+                qx.qx_gemm(pw.desc, pw.data, self.batch, self.x[xi], y, stream)
 
 
 def gated_kernel_durations(launches, reps=3):
@@ -294,6 +300,43 @@ def bench_decode(args, qx):
                      "launches_timed": 20 * len(dom)},
     }
     return out
+
+
+def bench_decode_batch(args, qx):
+    """The fused decode step for m = 2, 3, 4 sequences decoded together (one qx_gemm per
+    launch); one line per m, and batch 1 (qx_gemv) for reference."""
+    import torch
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    plan = configs.c4_plan(32)
+    quant = quantize_plan(plan)
+    stream = torch.cuda.Stream()
+    lines = []
+    base_us = None
+    for m in (1, 2, 3, 4):
+        step = DecodeStep(qx, dev, plan, quant, fused=True, batch=m)
+        ms = time_graph(step.launch, stream, args.steps, args.warmup)
+        us = ms * 1e3
+        base_us = us if m == 1 else base_us
+        log(f"decode step, batch {m}: {us:.1f} us")
+        lines.append({
+            "metric": "decode step tokens/s at batch m (7B decoder, 224 products per step)",
+            "value": round(m / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+            "data": "synthetic (seeded Philox weights and activations)",
+            "config": {"workload": f"7B decoder decode step, batch {m}: the decode7b matrices, "
+                                   "q|k|v and gate|up fused, 128 launches of "
+                                   + ("qx_gemv" if m == 1 else f"qx_gemm with m={m}")
+                                   + ", HIP graph replay",
+                       "batch": m, "packed_bytes_per_step": step.packed_bytes},
+            "us_per_step": round(us, 2),
+            "effective_weight_GBps": round(step.packed_bytes / (ms * 1e-3) / 1e9, 1),
+            "step_time_vs_batch1": round(us / base_us, 3),
+        })
+        del step
+        torch.cuda.empty_cache()
+    return lines
 
 
 def rotated_copies(qx, spec, device, min_total=512 << 20):
@@ -458,7 +501,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "c1", "c2", "c3", "c5", "q4x", "a8", "counters", "floor"])
+                    choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "q4x", "a8", "counters",
+                             "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -485,6 +529,9 @@ def main():
         print(json.dumps(bench_kernel_counters(args, qx)), flush=True)
     elif args.workload == "floor":
         print(json.dumps(bench_floor(args, qx)), flush=True)
+    elif args.workload == "batch":
+        for line in bench_decode_batch(args, qx):
+            print(json.dumps(line), flush=True)
     elif args.workload == "c5":
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)

@@ -35,4 +35,13 @@ int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, 
 int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
                    hipStream_t s);
 
+// Products of at most QX_MULTI_MAX_M rows may run GEMV-style (gemv_multi_applies
+// decides; launch_gemv_multi takes 2 <= m <= QX_MULTI_MAX_M, any k, not Q4X).
+#ifndef QX_MULTI_MAX_M
+#define QX_MULTI_MAX_M 4
+#endif
+bool gemv_multi_applies(const qx_desc* d, int m);
+int launch_gemv_multi(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y,
+                      hipStream_t s);
+
 }  // namespace qx

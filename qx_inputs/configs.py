@@ -101,6 +101,12 @@ def c4_activation(layer: int, t: int) -> np.ndarray:
     return activations(3, 1000 + 4 * layer + t, MLP if t == 3 else HIDDEN)
 
 
+def c4_batch_activations(layer: int, t: int, m: int) -> np.ndarray:
+    """[m][k] activations of m sequences decoded together; row 0 is c4_activation(layer, t)."""
+    count = MLP if t == 3 else HIDDEN
+    return np.stack([activations(3, 1000 + 4 * layer + t + 4096 * r, count) for r in range(m)])
+
+
 def c4_plan(layers: int = LAYERS) -> List[tuple]:
     """(spec, activation index) for every GEMV of one decode step, in launch order."""
     return [(c4_matrix(l, m), (l, DECODER_X[m])) for l in range(layers) for m in DECODER_MATS]

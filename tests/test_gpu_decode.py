@@ -72,3 +72,31 @@ def test_fused_and_single_launch_plans_agree(decode_steps):
             assert oracle.normwise_rel_err(a, b.astype(np.float64)) <= TOL, spec.name
         else:
             assert np.array_equal(a.view(np.uint16), b.view(np.uint16)), spec.name
+
+
+@pytest.mark.parametrize("m", [2, 4])
+def test_batched_decode_step_sampled_rows_match_oracle(gpu, decode_steps, m):
+    """The fused decode step for m sequences (qx_gemm per launch: the small-batch kernel
+    or the matrix-core GEMM, as the library routes each shape), graph replay; sampled
+    rows of the first two layers against the oracle for every sequence."""
+    import torch
+    import bench
+    plan, quant, _, _ = decode_steps
+    step = bench.DecodeStep(gpu, torch.device("cuda:0"), plan, quant, fused=True, batch=m)
+    bench.time_graph(step.launch, torch.cuda.Stream(), steps=2, warmup=1)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(m)
+    for i, (spec, (layer, t)) in enumerate(plan[:14]):
+        q = quant[i]
+        rows = np.sort(rng.choice(spec.n, SAMPLED_ROWS, replace=False))
+        w16 = oracle.dequant(q.codes[rows], q.group, q.kind,
+                             None if q.scales is None else q.scales[rows],
+                             None if q.zeros is None else q.zeros[rows],
+                             None if q.codebook is None else q.codebook[rows])
+        X = configs.c4_batch_activations(layer, t, m)
+        Y = step.output(i).cpu().numpy()
+        for r in range(m):
+            err = oracle.normwise_rel_err(Y[r][rows], oracle.gemv(w16, X[r]))
+            assert err <= TOL, (spec.name, r, err)
+    del step
+    torch.cuda.empty_cache()

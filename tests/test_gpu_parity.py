@@ -128,7 +128,7 @@ def test_gemv_configs(gpu, make):
     assert err <= TOL, err
 
 
-GEMM_M = [1, 3, 16, 17, 33, 64, 65]
+GEMM_M = [1, 2, 3, 4, 5, 16, 17, 33, 64, 65]
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
@@ -144,6 +144,42 @@ def test_gemm_matches_oracle(gpu, fmt, m):
     ref = oracle.gemm(X, _ref_w16(q))
     for r in range(m):
         assert oracle.normwise_rel_err(Y[r], ref[r]) <= TOL, r
+
+
+SMALL_BATCH = [(4096, 4096), (11008, 4096), (4096, 11008), (37, 1152), (9, 128), (130, 8192)]
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("m", [2, 3, 4])
+@pytest.mark.parametrize("shape", SMALL_BATCH, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_gemm_small_batch(gpu, fmt, m, shape):
+    """2 <= m <= 4: the GEMV-style small-batch kernel (every code decoded once and
+    multiplied with each activation row) where the library routes it (m = 2, or k > n),
+    else the matrix-core GEMM; rows of the oracle one by one."""
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = shape
+    print(f"gemm small batch {fmt} {shape} m={m}", flush=True)
+    q = random_quant(n, k, bits, g, kind, seed=n + k + m) if n * k > 10**7 else \
+        realistic_quant(n, k, bits, g, kind, seed=n + k + m)
+    X = activations(k, seed=m + 5, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    w16 = _ref_w16(q)
+    rows = np.arange(n) if n <= 4096 else np.sort(np.random.default_rng(m).choice(n, 2048, replace=False))
+    for r in range(m):
+        ref = oracle.gemv(w16[rows], X[r])
+        assert oracle.normwise_rel_err(Y[r][rows], ref) <= TOL, r
+
+
+def test_gemm_one_row_is_the_gemv(gpu):
+    """m = 1 runs the batch-1 GEMV: the same bits as qx_gemv."""
+    qx = gpu
+    q = realistic_quant(300, 4096, 4, 128, 0, seed=4)
+    pw = _pack(qx, q)
+    x = activations(4096, seed=2)
+    a = pw.gemm(to_dev(x[None, :])).cpu().numpy()[0]
+    b = pw.gemv(to_dev(x)).cpu().numpy()
+    assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
 
 
 @pytest.mark.parametrize("m", [16, 64, 512])
