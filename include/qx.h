@@ -75,8 +75,7 @@ enum {
   QX_E_ARG = -1,          /* null or misaligned pointer, malformed descriptor or table */
   QX_E_UNSUPPORTED = -2,  /* well-formed but not built (e.g. bits = 2, group = 256) */
   QX_E_SIZE = -3,         /* output capacity too small */
-  QX_E_HIP = -4,          /* the HIP runtime refused the launch */
-  QX_E_TIMEOUT = -5       /* a chain barrier wait exceeded its limit (qx_chain_status) */
+  QX_E_HIP = -4           /* the HIP runtime refused the launch */
 };
 
 /*
@@ -185,70 +184,6 @@ int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t
  */
 int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
             hipStream_t stream);
-
-/*
- * GEMV chains -- the products of one decode step in a single persistent launch.
- * Passage: decoding is memory-bound and the kernels decide its runtime (Section
- * 2.4); a decoder step is a fixed sequence of products whose formats differ per
- * layer type (mixed precision, Section 2.2). Launching each product separately
- * costs a dispatch and a ramp of the memory pipeline per product; a chain keeps
- * the GPU streaming weights between products.
- *
- * One product of the chain: y = W' x, as qx_gemv, with device pointers.
- * Products run in table order; product i starts after every product before it
- * has finished and its stores are visible, so x of a product may be the y of an
- * earlier one. y must not overlap x or packed of the same product.
- */
-typedef struct {
-  qx_desc desc;
-  const void* packed;
-  const uint16_t* x;
-  uint16_t* y;
-} qx_gemv_op;
-
-#define QX_CHAIN_HEADER_BYTES 4096
-
-/* Bytes of chain workspace for `count` products: a 4096-byte header (barrier
- * counters and the error flag) followed by the product table. */
-size_t qx_chain_workspace_size(int32_t count);
-
-/*
- * qx_chain_prepare -- validate a product table and write it, with a fresh
- * header, into `workspace` (device memory of at least
- * qx_chain_workspace_size(count) bytes, 256-byte aligned, owned by the caller).
- *   ops  host array of `count` products (count >= 1). Each descriptor must be
- *        valid for qx_gemv, not QX_Q4X, with k = 128*32 or 128*33 .. 128*88;
- *        packed and x 16-byte aligned, y 2-byte aligned.
- *   plan receives the kernel variant for this table's formats (pass it to
- *        qx_chain_run): chains of one format, or of 3-bit codebook and 4-bit
- *        uniform groups of 128, get a kernel compiled for exactly those.
- * Copies through a temporary host buffer and synchronizes `stream`. Returns
- * QX_E_ARG / QX_E_UNSUPPORTED for a bad or unsupported product (nothing written)
- * and QX_E_SIZE when ws_bytes is too small.
- */
-int qx_chain_prepare(const qx_gemv_op* ops, int32_t count, void* workspace, size_t ws_bytes,
-                     uint32_t* plan, hipStream_t stream);
-
-/*
- * qx_chain_run -- run a prepared chain (device; one cooperative launch).
- *   workspace  as prepared; count and plan as prepare left them (a mismatch
- *              makes the chain give up at once, flagging QX_E_TIMEOUT).
- *   spin_limit polls that find a barrier still closed before the chain gives up
- *              (0: 2^20, far beyond any real wait; 1: give up at the first closed
- *              poll, for tests of the error path). A chain that gives up flags QX_E_TIMEOUT
- *              in the workspace, and every block exits; prepare it again before
- *              the next run.
- * Results are those of qx_gemv on each product (same formats and accumulation
- * order class: fp16 products, fp32 sums in a fixed order, deterministic), within
- * the qx_gemv tolerance of the oracle. Calls that overlap on one workspace race.
- * The launch needs every block resident at once; QX_E_HIP if the device refuses.
- */
-int qx_chain_run(void* workspace, int32_t count, uint32_t plan, uint32_t spin_limit,
-                 hipStream_t stream);
-
-/* Synchronize `stream` and report whether the last run on `workspace` completed
- * (QX_OK) or gave up at a barrier (QX_E_TIMEOUT). */
-int qx_chain_status(const void* workspace, hipStream_t stream);
 
 /* Static string for a status code ("unknown status" for values not listed). */
 const char* qx_status_str(int status);

@@ -13,10 +13,6 @@ Functions keep the C names:
   qx_gemv(desc, packed, x, y, stream=None)
   qx_gemv_a8(desc, packed, x, y, stream=None)
   qx_gemm(desc, packed, m, X, Y, stream=None)
-  qx_chain_workspace_size(count)
-  qx_chain_prepare(ops, workspace, stream=None) -> plan   (ops: [(desc, packed, x, y), ...])
-  qx_chain_run(workspace, count, plan, spin_limit=0, stream=None)
-  qx_chain_status(workspace, stream=None) -> status
   qx_status_str(status)
 Tensor arguments are torch CUDA tensors (HIP device memory); ``stream`` is a
 torch stream (default: the current stream).
@@ -33,8 +29,7 @@ from . import _build
 
 QX_UNIFORM, QX_CODEBOOK, QX_Q4X = 0, 1, 2
 QX_OUT_F16, QX_OUT_CODES = 0, 1
-QX_OK, QX_E_ARG, QX_E_UNSUPPORTED, QX_E_SIZE, QX_E_HIP, QX_E_TIMEOUT = 0, -1, -2, -3, -4, -5
-QX_CHAIN_HEADER_BYTES = 4096
+QX_OK, QX_E_ARG, QX_E_UNSUPPORTED, QX_E_SIZE, QX_E_HIP = 0, -1, -2, -3, -4
 
 LIB_PATH = _build.LIB
 
@@ -46,12 +41,6 @@ class QxDesc(ctypes.Structure):
     def __repr__(self):
         return (f"QxDesc(n={self.n}, k={self.k}, bits={self.bits}, group={self.group}, "
                 f"kind={self.kind}, flags={self.flags})")
-
-
-class QxGemvOp(ctypes.Structure):
-    """One product of a GEMV chain (qx_gemv_op): device pointers."""
-    _fields_ = [("desc", QxDesc), ("packed", ctypes.c_void_p), ("x", ctypes.c_void_p),
-                ("y", ctypes.c_void_p)]
 
 
 def desc(n: int, k: int, bits: int, group: int, kind: int, flags: int = 0) -> QxDesc:
@@ -95,15 +84,6 @@ def load():
         L.qx_gemv_a8.restype = ctypes.c_int
         L.qx_gemm.argtypes = [D, P, ctypes.c_int32, P, P, P]
         L.qx_gemm.restype = ctypes.c_int
-        L.qx_chain_workspace_size.argtypes = [ctypes.c_int32]
-        L.qx_chain_workspace_size.restype = sz
-        L.qx_chain_prepare.argtypes = [ctypes.POINTER(QxGemvOp), ctypes.c_int32, P, sz,
-                                       ctypes.POINTER(ctypes.c_uint32), P]
-        L.qx_chain_prepare.restype = ctypes.c_int
-        L.qx_chain_run.argtypes = [P, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint32, P]
-        L.qx_chain_run.restype = ctypes.c_int
-        L.qx_chain_status.argtypes = [P, P]
-        L.qx_chain_status.restype = ctypes.c_int
         L.qx_status_str.argtypes = [ctypes.c_int]
         L.qx_status_str.restype = ctypes.c_char_p
         _lib = L
@@ -198,49 +178,6 @@ def qx_gemv_a8(d: QxDesc, packed, x, y, stream=None) -> None:
 def qx_gemm(d: QxDesc, packed, m: int, X, Y, stream=None) -> None:
     _check(load().qx_gemm(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(X), _dev_ptr(Y),
                           _stream(stream)), "qx_gemm")
-
-
-def qx_chain_workspace_size(count: int) -> int:
-    return int(load().qx_chain_workspace_size(int(count)))
-
-
-def qx_chain_prepare(ops, workspace, stream=None) -> int:
-    """Write the product table of ``ops`` ([(desc, packed, x, y), ...], device tensors
-    or raw device addresses) into ``workspace`` (a device tensor); returns the plan."""
-    arr = (QxGemvOp * len(ops))()
-    for i, (d, packed, x, y) in enumerate(ops):
-        addr = lambda t: t if isinstance(t, int) else t.data_ptr()
-        arr[i] = QxGemvOp(d, addr(packed), addr(x), addr(y))
-    plan = ctypes.c_uint32(0)
-    _check(load().qx_chain_prepare(arr, len(ops), _dev_ptr(workspace), workspace.nbytes,
-                                   ctypes.byref(plan), _stream(stream)), "qx_chain_prepare")
-    return plan.value
-
-
-def qx_chain_run(workspace, count: int, plan: int, spin_limit: int = 0, stream=None) -> None:
-    _check(load().qx_chain_run(_dev_ptr(workspace), int(count), int(plan), int(spin_limit),
-                               _stream(stream)), "qx_chain_run")
-
-
-def qx_chain_status(workspace, stream=None) -> int:
-    return int(load().qx_chain_status(_dev_ptr(workspace), _stream(stream)))
-
-
-class GemvChain:
-    """A prepared chain of GEMVs in a device workspace it owns (see qx_chain_prepare)."""
-
-    def __init__(self, ops, device="cuda", stream=None):
-        import torch
-        self.count = len(ops)
-        self.workspace = torch.zeros(qx_chain_workspace_size(self.count), dtype=torch.uint8,
-                                     device=device)
-        self.plan = qx_chain_prepare(ops, self.workspace, stream)
-
-    def run(self, stream=None, spin_limit: int = 0) -> None:
-        qx_chain_run(self.workspace, self.count, self.plan, spin_limit, stream)
-
-    def status(self, stream=None) -> int:
-        return qx_chain_status(self.workspace, stream)
 
 
 # ------------------------------------------------------------- conveniences

@@ -81,7 +81,6 @@ const char* qx_status_str(int st) {
     case QX_E_UNSUPPORTED: return "unsupported configuration";
     case QX_E_SIZE: return "output buffer too small";
     case QX_E_HIP: return "HIP launch error";
-    case QX_E_TIMEOUT: return "chain barrier wait exceeded its limit";
     default: return "unknown status";
   }
 }
@@ -227,58 +226,3 @@ int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, 
 }
 
 }  // extern "C"
-
-size_t qx_chain_workspace_size(int32_t count) {
-  return QX_CHAIN_HEADER_BYTES + (count > 0 ? (size_t)count : 0) * sizeof(qx_gemv_op);
-}
-
-int qx_chain_prepare(const qx_gemv_op* ops, int32_t count, void* workspace, size_t ws_bytes,
-                     uint32_t* plan, hipStream_t stream) {
-  if (ops == nullptr || count < 1 || workspace == nullptr || plan == nullptr) return QX_E_ARG;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return QX_E_ARG;
-  if (ws_bytes < qx_chain_workspace_size(count)) return QX_E_SIZE;
-  for (int32_t i = 0; i < count; ++i) {
-    const qx_gemv_op& op = ops[i];
-    const int st = check_desc(&op.desc);
-    if (st != QX_OK) return st;
-    if (!qx::chain_op_supported(&op.desc)) return QX_E_UNSUPPORTED;
-    if (op.packed == nullptr || op.x == nullptr || op.y == nullptr) return QX_E_ARG;
-    if (!aligned16(op.packed) || !aligned16(op.x) || !aligned2(op.y)) return QX_E_ARG;
-  }
-  std::vector<char> host(qx_chain_workspace_size(count), 0);
-  const char* base = static_cast<const char*>(workspace);
-  uint32_t paths = 0;
-  for (int32_t i = 0; i < count; ++i) {  // pointers as offsets from the workspace
-    qx::ChainOp e;
-    e.desc = ops[i].desc;
-    e.desc.flags = (uint32_t)qx::chain_path(&ops[i].desc);
-    paths |= 1u << e.desc.flags;
-    e.packed = static_cast<const char*>(ops[i].packed) - base;
-    e.x = reinterpret_cast<const char*>(ops[i].x) - base;
-    e.y = reinterpret_cast<const char*>(ops[i].y) - base;
-    std::memcpy(host.data() + QX_CHAIN_HEADER_BYTES + (size_t)i * sizeof(e), &e, sizeof(e));
-  }
-  // header: arrive, done, error = 0; count; plan
-  const uint32_t head[2] = {(uint32_t)count, qx::chain_plan(paths)};
-  std::memcpy(host.data() + 12, head, sizeof(head));
-  if (hipMemcpyAsync(workspace, host.data(), host.size(), hipMemcpyHostToDevice, stream) != hipSuccess ||
-      hipStreamSynchronize(stream) != hipSuccess)
-    return QX_E_HIP;
-  *plan = head[1];
-  return QX_OK;
-}
-
-int qx_chain_run(void* workspace, int32_t count, uint32_t plan, uint32_t spin_limit, hipStream_t stream) {
-  if (workspace == nullptr || count < 1 || plan > 13) return QX_E_ARG;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return QX_E_ARG;
-  return qx::launch_chain(workspace, count, plan, spin_limit == 0 ? (1u << 20) : spin_limit, stream);
-}
-
-int qx_chain_status(const void* workspace, hipStream_t stream) {
-  if (workspace == nullptr) return QX_E_ARG;
-  uint32_t error = 0;
-  if (hipStreamSynchronize(stream) != hipSuccess ||
-      hipMemcpy(&error, static_cast<const char*>(workspace) + 8, 4, hipMemcpyDeviceToHost) != hipSuccess)
-    return QX_E_HIP;
-  return error == 0 ? QX_OK : QX_E_TIMEOUT;
-}

@@ -35,22 +35,6 @@ int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, 
 int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
                    hipStream_t s);
 
-// GEMV chains. In the workspace the product table holds byte offsets from the
-// workspace itself (a kernel argument, so every address derived from it is known
-// to be global memory and is accessed with global, not flat, instructions).
-struct ChainOp {
-  qx_desc desc;
-  int64_t packed, x, y;
-};
-static_assert(sizeof(ChainOp) == sizeof(qx_gemv_op), "chain table entry size");
-// Whether a product can be part of a chain; its path id (0..23: format and K
-// class, stored in the table entry's flags); the kernel variant (plan) that covers
-// a set of paths (bit per path id); and the persistent launch.
-bool chain_op_supported(const qx_desc* d);
-int chain_path(const qx_desc* d);
-uint32_t chain_plan(uint32_t paths);
-int launch_chain(void* ws, int count, uint32_t plan, uint32_t spin_limit, hipStream_t s);
-
 // Products of at most QX_MULTI_MAX_M rows may run GEMV-style (gemv_multi_applies
 // decides; launch_gemv_multi takes 2 <= m <= QX_MULTI_MAX_M, any k, not Q4X).
 #ifndef QX_MULTI_MAX_M

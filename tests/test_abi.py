@@ -245,46 +245,3 @@ def test_gemv_a8_rejects_before_launch():
     assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(24), P(16), None) == qx.QX_E_ARG
     z = qx.desc(0, 128, 4, 128, qx.QX_UNIFORM)
     assert lib.qx_gemv_a8(ctypes.byref(z), None, None, None, None) == qx.QX_OK
-
-
-def test_chain_workspace_size():
-    assert qx.qx_chain_workspace_size(1) == qx.QX_CHAIN_HEADER_BYTES + 48
-    assert qx.qx_chain_workspace_size(128) == qx.QX_CHAIN_HEADER_BYTES + 128 * 48
-    assert ctypes.sizeof(qx.QxGemvOp) == 48
-
-
-def test_chain_calls_reject_before_any_device_work():
-    """Every argument error of the chain calls is found on the host, before a copy or a
-    launch (no device memory exists here: the addresses are never dereferenced)."""
-    lib = qx.load()
-    P = ctypes.c_void_p
-    plan = ctypes.c_uint32(0)
-    ws, wsz = P(1 << 20), qx.qx_chain_workspace_size(4)
-
-    def prep(ops, ws=ws, wsz=wsz, plan_ptr=ctypes.byref(plan)):
-        arr = (qx.QxGemvOp * max(len(ops), 1))(*ops)
-        return lib.qx_chain_prepare(arr if ops else None, len(ops), ws, wsz, plan_ptr, None)
-
-    good = qx.QxGemvOp(qx.desc(64, 4096, 4, 128, 0), 1 << 12, 2 << 12, 3 << 12)
-    assert prep([]) == qx.QX_E_ARG
-    assert prep([good], ws=P(1 << 20 | 16)) == qx.QX_E_ARG            # workspace not 256-aligned
-    assert prep([good], ws=None) == qx.QX_E_ARG
-    assert prep([good], plan_ptr=None) == qx.QX_E_ARG
-    assert prep([good] * 5) == qx.QX_E_SIZE                          # 5 products, room for 4
-    for d in (qx.desc(64, 2048, 4, 128, 0),                          # C = 16: no chain path
-              qx.desc(64, 89 * 128, 4, 128, 0),                      # longer than 88 chunks
-              qx.desc(64, 4096, 4, 64, qx.QX_Q4X)):
-        assert prep([good, qx.QxGemvOp(d, 1 << 12, 2 << 12, 3 << 12)]) == qx.QX_E_UNSUPPORTED
-    assert prep([qx.QxGemvOp(qx.desc(64, 4096, 5, 128, 0), 1 << 12, 2 << 12, 3 << 12)]) == \
-        qx.QX_E_UNSUPPORTED
-    assert prep([qx.QxGemvOp(qx.desc(64, 4096, 4, 128, 0), 0, 2 << 12, 3 << 12)]) == qx.QX_E_ARG
-    assert prep([qx.QxGemvOp(qx.desc(64, 4096, 4, 128, 0), 1 << 12, (2 << 12) + 8, 3 << 12)]) == \
-        qx.QX_E_ARG
-    assert prep([qx.QxGemvOp(qx.desc(64, 4096, 4, 128, 0), 1 << 12, 2 << 12, (3 << 12) + 1)]) == \
-        qx.QX_E_ARG
-    assert lib.qx_chain_run(ws, 0, 0, 0, None) == qx.QX_E_ARG
-    assert lib.qx_chain_run(ws, 4, 14, 0, None) == qx.QX_E_ARG
-    assert lib.qx_chain_run(P(1 << 20 | 64), 4, 0, 0, None) == qx.QX_E_ARG
-    assert lib.qx_chain_run(None, 4, 0, 0, None) == qx.QX_E_ARG
-    assert lib.qx_chain_status(None, None) == qx.QX_E_ARG
-    assert qx.qx_status_str(qx.QX_E_TIMEOUT).startswith("chain barrier")
