@@ -175,12 +175,14 @@ int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t
                hipStream_t stream);
 
 /*
- * qx_gemm -- Y = X W'^T for m activation rows (device; prefill).
+ * qx_gemm -- Y = X W'^T for m activation rows (device; prefill and batched decode).
  * Passage: as qx_gemv, batched over m rows.
  *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte
- *   alignment suffices for Y). fp16 matrix-core products, fp32 accumulate,
- *   RNE to fp16. m = 0 or n = 0 is a no-op; m must be <= 65536.
- *   QX_Q4X matrices are not supported here (QX_E_UNSUPPORTED).
+ *   alignment suffices for Y). fp16 products, fp32 accumulate, RNE to fp16:
+ *   on the matrix cores with W' decoded exactly into their operands, or, for a
+ *   few rows (m <= 4, by shape and format), GEMV-style with every code decoded
+ *   once for all rows. m = 0 or n = 0 is a no-op; m must be <= 65536. All
+ *   formats, Q4X included.
  */
 int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
             hipStream_t stream);

@@ -46,7 +46,8 @@ constexpr int kXRowBytes = 272;  // one activation row of one chunk (fragment or
 template <int BITS, int KIND, int G>
 struct LaneCodes {
   static constexpr int kDw = BITS == 4 ? 4 : 7;
-  static constexpr int kMetaDw = KIND == QX_UNIFORM ? 128 / G : (128 / G) << (BITS - 1);
+  // Q4X: m[0] = the two groups' binary16 scales, m[1] = their selectors (bits 0-1, 2-3)
+  static constexpr int kMetaDw = KIND == QX_UNIFORM ? 128 / G : KIND == QX_Q4X ? 2 : (128 / G) << (BITS - 1);
   uint32_t d[kDw];  // b = 3: d[0..2] code dwords g, 4+g, 8+g; d[3..4] dwords 2g, 2g+1;
                     //        d[5..6] dwords 8+2(g&1), 9+2(g&1) (bit 2 of the spare codes)
   uint32_t m[kMetaDw];
@@ -59,8 +60,10 @@ template <int BITS, int KIND, int G, int SC>
 struct CodeTile {
   static constexpr int kRowBytes = BITS * SC * 16;
   static constexpr int kRowStride = kRowBytes + (272 - kRowBytes % 256) % 256;  // = 16 mod 256
-  static constexpr int kMetaRow = KIND == QX_UNIFORM ? SC * (128 / G) * 4 : SC * (128 / G) * (2 << BITS);
-  static constexpr int kMetaStride = kMetaRow + (KIND == QX_UNIFORM ? 4 : 16);
+  static constexpr int kMetaRow = KIND == QX_UNIFORM ? SC * (128 / G) * 4
+                                  : KIND == QX_Q4X  ? SC * 8
+                                                    : SC * (128 / G) * (2 << BITS);
+  static constexpr int kMetaStride = kMetaRow + (KIND == QX_UNIFORM ? 4 : KIND == QX_Q4X ? 8 : 16);
 };
 
 template <int BITS, int KIND, int G, int SC>
@@ -142,6 +145,9 @@ __device__ __forceinline__ h8_t decode_frag(const LaneCodes<BITS, KIND, G>& lc,
       uint32_t elo, ehi, olo, ohi;
       lut4_bytes(lut[gr], D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
       lut4_bytes(lut[gr], (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
+      if constexpr (KIND == QX_Q4X)  // fp16(s * CB[t][q]): one rounding, as qx_dequant
+        return frag(hmul2(perm(ehi, elo, 0x06020400u), gc.sp[gr]), hmul2(perm(ohi, olo, 0x06020400u), gc.sp[gr]),
+                    hmul2(perm(ehi, elo, 0x07030501u), gc.sp[gr]), hmul2(perm(ohi, olo, 0x07030501u), gc.sp[gr]));
       return frag(perm(ehi, elo, 0x06020400u), perm(ohi, olo, 0x06020400u),
                   perm(ehi, elo, 0x07030501u), perm(ohi, olo, 0x07030501u));
     }
@@ -219,7 +225,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   constexpr int kXBuf = KS * BM * kXRowBytes;
   constexpr int kCTotal = BN * BITS * SC;                                 // 16-byte code pieces
   constexpr int kCPieces = (kCTotal + kGemmThreads - 1) / kGemmThreads;  // per thread
-  constexpr int kMetaUnit = KIND == QX_UNIFORM ? 4 : 16;   // bytes per table load
+  constexpr int kMetaUnit = KIND == QX_UNIFORM ? 4 : KIND == QX_Q4X ? 8 : 16;  // bytes per table load
   constexpr int kMPieces = (BN * CT::kMetaRow / kMetaUnit + kGemmThreads - 1) / kGemmThreads;
   static_assert(KS * BM * 16 % kGemmThreads == 0, "activation pieces must divide evenly");
   static_assert(S % DX == 0, "activation register sets must divide the super-round");
@@ -227,6 +233,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   __shared__ __align__(16) char xs[2 * kXBuf];
   __shared__ __align__(16) char cts[BN * CT::kRowStride];
   __shared__ __align__(16) char mts[BN * CT::kMetaStride];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
 
   // Block -> (weight tile bn, activation tile bm). With several activation tiles,
   // the tiles of one weight tile go to one XCD (workgroups are dealt to the 8 XCDs
@@ -267,6 +274,16 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
       const int p = min((int)threadIdx.x + i * kGemmThreads, BN * kUnits - 1);
       const int ul = p % kUnits, rl = p / kUnits;
       const int row = min(n0 + rl, n - 1);
+      if constexpr (KIND == QX_Q4X) {
+        // chunk c of the row: the scales of groups 2c, 2c + 1 (one dword) and their
+        // selectors (4 bits of the row's selector word for groups 16(c/8) ..)
+        const int c = min(j * SC + ul, C - 1), W = (G_row + 15) / 16;
+        const uint32_t sc = *reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + 2 * c) * 2);
+        const uint32_t sw = *reinterpret_cast<const uint32_t*>(packed + meta_off + meta_off / 16 +
+                                                               ((size_t)row * W + c / 8) * 4);
+        mr[i] = u32x4{sc, (sw >> (4 * (c % 8))) & 0xFu, 0u, 0u};
+        continue;
+      }
       // group index of this unit, clamped to the row's last group
       const int gi = min(j * SC * (128 / G) + ul * kMetaUnit / (KIND == QX_UNIFORM ? 4 : 2 << BITS),
                          G_row - 1);
@@ -294,6 +311,8 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
         char* dst = mts + rl * CT::kMetaStride + ul * kMetaUnit;
         if constexpr (KIND == QX_UNIFORM)
           *reinterpret_cast<uint32_t*>(dst) = mr[i].x;
+        else if constexpr (KIND == QX_Q4X)
+          *reinterpret_cast<u32x2*>(dst) = u32x2{mr[i].x, mr[i].y};
         else
           *reinterpret_cast<u32x4*>(dst) = mr[i];
       }
@@ -331,6 +350,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f4_t{0.f, 0.f, 0.f, 0.f};
 
   u32x4 cr[kCPieces], mr[kMPieces];
+  if constexpr (KIND == QX_Q4X) stage_q4x_tables(packed + q4x_offsets(n, k).codebook, q4lut);
   load_codes(0, cr, mr);
   store_codes(cr, mr);
   // Activations: round r + DX is loaded into register set r % DX during round r, and
@@ -362,6 +382,14 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
           read_lane_codes<BITS, KIND, G, SC>(cur[nt], cts, mts, 16 * (ng * NT + nt) + li, u * KS + ks, g);
           if constexpr (KIND == QX_UNIFORM) {
             gc[nt] = group_consts<BITS, G>(cur[nt].m);
+          } else if constexpr (KIND == QX_Q4X) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {  // group i of the chunk: scale pair, sub-codebook tables
+              gc[nt].sp[i] = perm(cur[nt].m[0], cur[nt].m[0], i == 0 ? 0x01000100u : 0x03020302u);
+              const uint32_t* tp = q4lut + 8 * ((cur[nt].m[1] >> (2 * i)) & 3u);
+              const u32x4 tl = *reinterpret_cast<const u32x4*>(tp), th = *reinterpret_cast<const u32x4*>(tp + 4);
+              lut[nt][i] = LutGroup<4>{{tl.x, tl.y, tl.z, tl.w}, {th.x, th.y, th.z, th.w}};
+            }
           } else {
 #pragma unroll
             for (int i = 0; i < 128 / G; ++i) lut[nt][i] = lut_group<BITS>(&cur[nt].m[i << (BITS - 1)]);
@@ -480,6 +508,7 @@ int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, 
   QX_GEMM_CASE(3, 1, 32) QX_GEMM_CASE(3, 1, 64) QX_GEMM_CASE(3, 1, 128)
   QX_GEMM_CASE(4, 0, 32) QX_GEMM_CASE(4, 0, 64) QX_GEMM_CASE(4, 0, 128)
   QX_GEMM_CASE(4, 1, 32) QX_GEMM_CASE(4, 1, 64) QX_GEMM_CASE(4, 1, 128)
+  QX_GEMM_CASE(4, 2, 64)
 #undef QX_GEMM_CASE
   return QX_E_UNSUPPORTED;
 }

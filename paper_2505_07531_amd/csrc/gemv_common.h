@@ -310,18 +310,10 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
   }
 }
 
-// Q4X: the matrix's 4 x 16 binary16 codebook as the v_perm lookup tables of
-// lut4_bytes (per sub-codebook 4 dwords of low bytes, then 4 of high bytes),
-// written to LDS by the first 16 threads of the block.
+// Q4X: the matrix's codebook tables in LDS (see stage_q4x_tables).
 __device__ __forceinline__ void stage_q4x_lut(const char* __restrict__ packed, int n, int k,
                                               uint32_t* lut) {
-  if (threadIdx.x < 16) {
-    const int t = threadIdx.x >> 2, i = threadIdx.x & 3;
-    const uint32_t* cb = reinterpret_cast<const uint32_t*>(packed + q4x_offsets(n, k).codebook) + 8 * t;
-    const uint32_t w0 = cb[2 * i], w1 = cb[2 * i + 1];
-    lut[8 * t + i] = perm(w1, w0, 0x06040200u);
-    lut[8 * t + 4 + i] = perm(w1, w0, 0x07050301u);
-  }
+  stage_q4x_tables(packed + q4x_offsets(n, k).codebook, lut);
 }
 
 // Byte offset of the group sums after C chunks of x and n floats of partials.

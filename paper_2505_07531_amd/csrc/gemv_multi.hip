@@ -254,7 +254,8 @@ int launch_multi_t(const qx_desc* d, const void* packed, int m, const uint16_t* 
 // into matrix-core fragments at every m; at m = 2 so do 4-bit 64-code groups when
 // k <= n.
 bool gemv_multi_applies(const qx_desc* d, int m) {
-  if (m < 1 || m > QX_MULTI_MAX_M || d->kind == QX_Q4X) return false;
+  if (d->kind == QX_Q4X) return m == 1;  // the small-batch kernel has no Q4X path
+  if (m < 1 || m > QX_MULTI_MAX_M) return false;
   const bool cb4 = d->kind == QX_CODEBOOK && d->bits == 4;
   if (cb4 && d->group == 32) return false;
   if (m == 1 || d->k > d->n) return true;

@@ -215,7 +215,6 @@ int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, 
   const int st = check_desc(d);
   if (st != QX_OK) return st;
   if (m < 0 || m > 65536) return QX_E_ARG;
-  if (d->kind == QX_Q4X) return QX_E_UNSUPPORTED;
   if (m == 0 || d->n == 0) return QX_OK;
   if (packed == nullptr || X == nullptr || Y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(X) || !aligned2(Y)) return QX_E_ARG;

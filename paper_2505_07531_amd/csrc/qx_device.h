@@ -229,4 +229,17 @@ __device__ __forceinline__ float wave_sum(float v) {
   return dpp_plus<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
 }
 
+// Q4X: a matrix's 4 x 16 binary16 codebook (128 bytes at `codebook`) as the
+// v_perm lookup tables of lut4_bytes (per sub-codebook 4 dwords of low bytes, then
+// 4 of high bytes), written to LDS by the first 16 threads of the block.
+__device__ __forceinline__ void stage_q4x_tables(const char* __restrict__ codebook, uint32_t* lut) {
+  if (threadIdx.x < 16) {
+    const int t = threadIdx.x >> 2, i = threadIdx.x & 3;
+    const uint32_t* cb = reinterpret_cast<const uint32_t*>(codebook) + 8 * t;
+    const uint32_t w0 = cb[2 * i], w1 = cb[2 * i + 1];
+    lut[8 * t + i] = perm(w1, w0, 0x06040200u);
+    lut[8 * t + 4 + i] = perm(w1, w0, 0x07050301u);
+  }
+}
+
 }  // namespace qx

@@ -225,7 +225,8 @@ def test_q4x_device_calls_reject_before_launch():
     lib = qx.load()
     d = qx.desc(4, 128, 4, 64, qx.QX_Q4X)
     P = ctypes.c_void_p
-    assert lib.qx_gemm(ctypes.byref(d), P(16), 4, P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    assert lib.qx_gemm(ctypes.byref(d), P(16), 4, None, P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemm(ctypes.byref(d), P(16), -1, P(16), P(16), None) == qx.QX_E_ARG
     assert lib.qx_gemv(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
     assert lib.qx_dequant(ctypes.byref(d), P(8), 0, P(16), None) == qx.QX_E_ARG
     bad = qx.desc(4, 128, 4, 32, qx.QX_Q4X)

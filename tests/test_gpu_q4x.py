@@ -122,10 +122,37 @@ def test_q4x_max_k(gpu):
     assert oracle.normwise_rel_err(pw.gemv(to_dev(x)).cpu().numpy(), oracle.gemv(w16, x)) <= TOL
 
 
-def test_q4x_gemm_is_not_supported(gpu):
+GEMM_CASES = [(1, 40, 1152), (2, 40, 1152), (3, 130, 4096), (16, 100, 384), (17, 37, 11008),
+              (64, 300, 1024), (65, 64, 4096), (512, 260, 2048)]
+
+
+@pytest.mark.parametrize("m,n,k", GEMM_CASES, ids=lambda v: str(v))
+def test_q4x_gemm_matches_oracle(gpu, m, n, k):
+    """qx_gemm on Q4X (m = 1: the GEMV; else the matrix-core GEMM with W' decoded into
+    its operands as fp16(s * CB[t][q])): every output row within the parity bound."""
     qx = gpu
-    q = random_q4x(16, 256, seed=2)
-    pw = _pack(qx, q)
-    with pytest.raises(qx.QxError) as e:
-        pw.gemm(to_dev(activations(256, seed=1, m=4)))
-    assert e.value.status == qx.QX_E_UNSUPPORTED
+    print(f"q4x gemm m={m} {n}x{k}", flush=True)
+    q = random_q4x(n, k, seed=m * 7 + n) if m % 2 else realistic_q4x(n, k, seed=m + n)
+    X = activations(k, seed=m + 3, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    w = _ref(q)
+    for r in range(m):
+        assert oracle.normwise_rel_err(Y[r], oracle.gemv(w, X[r])) <= TOL, r
+
+
+def test_q4x_gemm_one_hot_rows_are_columns_of_w(gpu):
+    """Each activation row one-hot at a different position: the product is exact, so row r
+    of Y is column j_r of W' bit for bit, zeros up to sign (checks the fragment decode,
+    scales and selectors of every group the rows touch)."""
+    qx = gpu
+    n, k, m = 64, 4096, 64
+    q = random_q4x(n, k, seed=11)
+    cols = np.random.default_rng(3).choice(k, m, replace=False)
+    X = np.zeros((m, k), np.float16)
+    X[np.arange(m), cols] = 1.0
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    w = _ref(q)
+    ref = w[:, cols].T.copy()
+    assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))  # +0 sums of a -0 weight
+    nz = ref.astype(np.float32) != 0
+    assert np.array_equal(Y.view(np.uint16)[nz], ref.view(np.uint16)[nz])
