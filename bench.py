@@ -16,7 +16,8 @@ and the CPU oracle timed on a bounded sample.
 Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
 --workload batch (the same decode step for 1 to 4 sequences decoded together,
-one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workload q4x (the paper's Q4X
+one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workload c5a8 (the same with int8
+per-token activations), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
 rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
 matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
@@ -39,6 +40,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, published
 FP16_MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 matrix-core peak, published
+INT8_MFMA_PEAK_TOPS = 5000.0    # dense int8 matrix-core peak, published
 METRIC = "batch-1 qGEMV effective HBM GB/s (% of peak) + µs per 7B decode step"
 KERNEL_SOURCES = ["qx_device.h", "gemv_common.h", "gemv.hip", "gemm.hip", "dequant.hip"]
 
@@ -392,7 +394,9 @@ def bench_single_gemv(args, qx, name, a8=False):
                          "avg_launch_us": round(ms * 1e3, 3)}}
 
 
-def bench_gemm(args, qx):
+def bench_gemm(args, qx, a8=False):
+    """c5 prefill: gate, up, down at m = 16, 64, 512. a8: activations quantized per token
+    (qx_quantize_a8, once per input, inside the timed region) and qx_gemm_a8."""
     import torch
     from qx_inputs import configs
     dev = torch.device("cuda:0")
@@ -408,8 +412,17 @@ def bench_gemm(args, qx):
         xin, xdn = configs.c5_activations(m)
         xi, xd = torch.from_numpy(xin).to(dev), torch.from_numpy(xdn).to(dev)
         ys = {nm: torch.empty((m, mats[nm].desc.n), dtype=torch.float16, device=dev) for nm in mats}
+        qi_, si_ = torch.empty(xi.shape, dtype=torch.int8, device=dev), torch.empty(m, dtype=torch.float32, device=dev)
+        qd_, sd_ = torch.empty(xd.shape, dtype=torch.int8, device=dev), torch.empty(m, dtype=torch.float32, device=dev)
         def launch_all():
             for st in sets:
+                if a8:
+                    qx.qx_quantize_a8(m, xi.shape[1], xi, qi_, si_)
+                    qx.qx_quantize_a8(m, xd.shape[1], xd, qd_, sd_)
+                    for nm in ("gate", "up", "down"):
+                        dn = nm == "down"
+                        qx.qx_gemm_a8(mats[nm].desc, st[nm], m, qd_ if dn else qi_, sd_ if dn else si_, ys[nm])
+                    continue
                 for nm in ("gate", "up", "down"):
                     qx.qx_gemm(mats[nm].desc, st[nm], m, xd if nm == "down" else xi, ys[nm])
         # ms for the three GEMMs
@@ -418,18 +431,23 @@ def bench_gemm(args, qx):
         byts = sum(configs.c5_matrix(nm).packed_bytes for nm in mats) + m * 90_624
         tf = flops / (t * 1e-3) / 1e12
         gbs = byts / (t * 1e-3) / 1e9
-        hbm_t, mfma_t = byts / (HBM_PEAK_GBS * 1e9), flops / (FP16_MFMA_PEAK_TFLOPS * 1e12)
+        peak = INT8_MFMA_PEAK_TOPS if a8 else FP16_MFMA_PEAK_TFLOPS
+        hbm_t, mfma_t = byts / (HBM_PEAK_GBS * 1e9), flops / (peak * 1e12)
         bound = "hbm" if hbm_t >= mfma_t else "mfma"
         frac = (hbm_t if bound == "hbm" else mfma_t) / (t * 1e-3)
-        lines.append({"metric": f"prefill qGEMM (gate+up+down, m={m})", "value": round(tf, 3),
-                      "unit": "TFLOP/s", "n_gpus": 1, "steps": 3 * nsets, "warmup": nsets,
-                      "ms_per_step": round(t, 6), "higher_is_better": True, "scaling": "weak",
-                      "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        unit = "TOP/s" if a8 else "TFLOP/s"
+        lines.append({"metric": f"prefill qGEMM{' W·A8' if a8 else ''} (gate+up+down, m={m})",
+                      "value": round(tf, 3), "unit": unit, "n_gpus": 1, "steps": 3 * nsets,
+                      "warmup": nsets, "ms_per_step": round(t, 6), "higher_is_better": True,
+                      "scaling": "weak", "vs_baseline": None, "dtype": "i8" if a8 else "f16",
+                      "data": "synthetic",
                       "config": {"workload": f"c5 MLP prefill GEMM m={m}, 3-bit uniform g64, "
-                                             f"graph over {nsets} copies of the three matrices"},
+                                             + ("int8 per-token activations (quantized in the timed "
+                                                "region), " if a8 else "")
+                                             + f"graph over {nsets} copies of the three matrices"},
                       "roofline": {"bound": bound, "achieved": round(gbs if bound == "hbm" else tf, 2),
-                                   "peak": HBM_PEAK_GBS if bound == "hbm" else FP16_MFMA_PEAK_TFLOPS,
-                                   "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                                   "peak": HBM_PEAK_GBS if bound == "hbm" else peak,
+                                   "unit": "GB/s" if bound == "hbm" else unit,
                                    "frac": round(frac, 4), "traffic": None}})
     return lines
 
@@ -501,8 +519,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "q4x", "a8", "counters",
-                             "floor"])
+                    choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "c5a8", "q4x", "a8",
+                             "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -531,6 +549,9 @@ def main():
         print(json.dumps(bench_floor(args, qx)), flush=True)
     elif args.workload == "batch":
         for line in bench_decode_batch(args, qx):
+            print(json.dumps(line), flush=True)
+    elif args.workload == "c5a8":
+        for line in bench_gemm(args, qx, a8=True):
             print(json.dumps(line), flush=True)
     elif args.workload == "c5":
         for line in bench_gemm(args, qx):
