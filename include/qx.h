@@ -175,6 +175,34 @@ int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t
                hipStream_t stream);
 
 /*
+ * qx_quantize_a8 -- per-token 8-bit activations for qx_gemm_a8 (device).
+ * Passage: activations quantized to 8 bits by round-to-nearest, one scale per
+ * token (Section 2.4; the W3A8 rows of Table 1, Table 2's runs).
+ *   X fp16 [m][k] row-major, finite, 16-byte aligned; k a positive multiple of
+ *   128 (at most 1 << 20), 0 <= m <= 65536.
+ *   Xq int8 [m][k] (written, 16-byte aligned), sx fp32 [m] (written), per row
+ *   exactly as qx_gemv_a8 quantizes its vector: amax = max|x|, xq = nearest
+ *   integer to x * fp32(127/amax) (the product exact), sx = fp32(amax/127);
+ *   an all-zero row gives xq = 0, sx = 0.
+ * The codes of one X can feed every product that reads that X (q, k and v, or
+ * gate and up). QX_E_ARG for bad sizes, null or misaligned pointers.
+ */
+int qx_quantize_a8(int32_t m, int32_t k, const uint16_t* X, int8_t* Xq, float* sx,
+                   hipStream_t stream);
+
+/*
+ * qx_gemm_a8 -- Y = X W'^T with 8-bit activations (device; uniform kind).
+ * Passage: as qx_gemv_a8, for m activation rows (prefill of a W3A8 model).
+ *   Xq, sx as qx_quantize_a8 wrote them for the same k; Y fp16 [m][n]
+ *   (written, 2-byte aligned) = sx[r] * sum_j s_j * sum_{k in group j}
+ *   (q - z_j) * xq[r][k], the group sums exact (int8 matrix-core products,
+ *   int32 accumulation), scaled in fp32, rounded to nearest-even.
+ * Codebook and Q4X descriptors: QX_E_UNSUPPORTED. m = 0 or n = 0 is a no-op.
+ */
+int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq, const float* sx,
+               uint16_t* Y, hipStream_t stream);
+
+/*
  * qx_gemm -- Y = X W'^T for m activation rows (device; prefill and batched decode).
  * Passage: as qx_gemv, batched over m rows.
  *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte

@@ -13,6 +13,8 @@ Functions keep the C names:
   qx_gemv(desc, packed, x, y, stream=None)
   qx_gemv_a8(desc, packed, x, y, stream=None)
   qx_gemm(desc, packed, m, X, Y, stream=None)
+  qx_quantize_a8(m, k, X, Xq, sx, stream=None)
+  qx_gemm_a8(desc, packed, m, Xq, sx, Y, stream=None)
   qx_status_str(status)
 Tensor arguments are torch CUDA tensors (HIP device memory); ``stream`` is a
 torch stream (default: the current stream).
@@ -84,6 +86,10 @@ def load():
         L.qx_gemv_a8.restype = ctypes.c_int
         L.qx_gemm.argtypes = [D, P, ctypes.c_int32, P, P, P]
         L.qx_gemm.restype = ctypes.c_int
+        L.qx_quantize_a8.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P]
+        L.qx_quantize_a8.restype = ctypes.c_int
+        L.qx_gemm_a8.argtypes = [D, P, ctypes.c_int32, P, P, P, P]
+        L.qx_gemm_a8.restype = ctypes.c_int
         L.qx_status_str.argtypes = [ctypes.c_int]
         L.qx_status_str.restype = ctypes.c_char_p
         _lib = L
@@ -180,6 +186,26 @@ def qx_gemm(d: QxDesc, packed, m: int, X, Y, stream=None) -> None:
                           _stream(stream)), "qx_gemm")
 
 
+def qx_quantize_a8(m: int, k: int, X, Xq, sx, stream=None) -> None:
+    _check(load().qx_quantize_a8(int(m), int(k), _dev_ptr(X), _dev_ptr(Xq), _dev_ptr(sx),
+                                 _stream(stream)), "qx_quantize_a8")
+
+
+def qx_gemm_a8(d: QxDesc, packed, m: int, Xq, sx, Y, stream=None) -> None:
+    _check(load().qx_gemm_a8(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(Xq), _dev_ptr(sx),
+                             _dev_ptr(Y), _stream(stream)), "qx_gemm_a8")
+
+
+def quantize_a8(X, stream=None):
+    """(Xq int8 [m][k], sx fp32 [m]) of an fp16 [m][k] device tensor."""
+    import torch
+    m, k = X.shape
+    Xq = torch.empty((m, k), dtype=torch.int8, device=X.device)
+    sx = torch.empty(m, dtype=torch.float32, device=X.device)
+    qx_quantize_a8(m, k, X, Xq, sx, stream)
+    return Xq, sx
+
+
 # ------------------------------------------------------------- conveniences
 class PackedWeight:
     """A packed matrix resident in device memory, with its descriptor."""
@@ -212,6 +238,14 @@ class PackedWeight:
             y = torch.empty(self.desc.n, dtype=torch.float16, device=x.device)
         qx_gemv(self.desc, self.data, x, y, stream)
         return y
+
+    def gemm_a8(self, Xq, sx, Y=None, stream=None):
+        import torch
+        m = Xq.shape[0]
+        if Y is None:
+            Y = torch.empty((m, self.desc.n), dtype=torch.float16, device=Xq.device)
+        qx_gemm_a8(self.desc, self.data, m, Xq, sx, Y, stream)
+        return Y
 
     def gemv_a8(self, x, y=None, stream=None):
         import torch

@@ -210,6 +210,27 @@ int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t
   return qx::launch_gemv_a8(d, packed, x, y, stream);
 }
 
+int qx_quantize_a8(int32_t m, int32_t k, const uint16_t* X, int8_t* Xq, float* sx, hipStream_t stream) {
+  if (m < 0 || m > 65536 || k <= 0 || k % 128 != 0 || k > kMaxK) return QX_E_ARG;
+  if (m == 0) return QX_OK;
+  if (X == nullptr || Xq == nullptr || sx == nullptr) return QX_E_ARG;
+  if (!aligned16(X) || !aligned16(Xq) || (reinterpret_cast<uintptr_t>(sx) & 3u) != 0) return QX_E_ARG;
+  return qx::launch_quantize_a8(m, k, X, Xq, sx, stream);
+}
+
+int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq, const float* sx,
+               uint16_t* Y, hipStream_t stream) {
+  const int st = check_desc(d);
+  if (st != QX_OK) return st;
+  if (m < 0 || m > 65536) return QX_E_ARG;
+  if (d->kind != QX_UNIFORM) return QX_E_UNSUPPORTED;
+  if (m == 0 || d->n == 0) return QX_OK;
+  if (packed == nullptr || Xq == nullptr || sx == nullptr || Y == nullptr) return QX_E_ARG;
+  if (!aligned16(packed) || !aligned16(Xq) || (reinterpret_cast<uintptr_t>(sx) & 3u) != 0 || !aligned2(Y))
+    return QX_E_ARG;
+  return qx::launch_gemm_a8(d, packed, m, Xq, sx, Y, stream);
+}
+
 int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
             hipStream_t stream) {
   const int st = check_desc(d);

@@ -35,6 +35,12 @@ int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, 
 int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
                    hipStream_t s);
 
+// W·A8 for many rows: per-row int8 activations and the integer-product GEMM
+// (uniform descriptors).
+int launch_quantize_a8(int m, int k, const uint16_t* X, int8_t* Xq, float* sx, hipStream_t s);
+int launch_gemm_a8(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
+                   hipStream_t s);
+
 // Products of at most QX_MULTI_MAX_M rows may run GEMV-style (gemv_multi_applies
 // decides; launch_gemv_multi takes 2 <= m <= QX_MULTI_MAX_M, any k, not Q4X).
 #ifndef QX_MULTI_MAX_M

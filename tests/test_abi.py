@@ -246,3 +246,22 @@ def test_gemv_a8_rejects_before_launch():
     assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(24), P(16), None) == qx.QX_E_ARG
     z = qx.desc(0, 128, 4, 128, qx.QX_UNIFORM)
     assert lib.qx_gemv_a8(ctypes.byref(z), None, None, None, None) == qx.QX_OK
+
+
+def test_a8_gemm_calls_reject_before_launch():
+    lib = qx.load()
+    P = ctypes.c_void_p
+    d = qx.desc(64, 4096, 3, 128, 0)
+    assert lib.qx_quantize_a8(4, 4000, P(16), P(16), P(16), None) == qx.QX_E_ARG   # k % 128
+    assert lib.qx_quantize_a8(-1, 4096, P(16), P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_quantize_a8(4, 4096, None, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_quantize_a8(4, 4096, P(16), P(24), P(16), None) == qx.QX_E_ARG  # Xq alignment
+    assert lib.qx_quantize_a8(4, 4096, P(16), P(16), P(18), None) == qx.QX_E_ARG  # sx alignment
+    assert lib.qx_quantize_a8(0, 4096, None, None, None, None) == qx.QX_OK
+    for kind, bits, group in ((qx.QX_CODEBOOK, 3, 128), (qx.QX_Q4X, 4, 64)):
+        bad = qx.desc(64, 4096, bits, group, kind)
+        assert lib.qx_gemm_a8(ctypes.byref(bad), P(16), 4, P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+    assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 4, None, P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 4, P(16), P(16), P(17), None) == qx.QX_E_ARG
+    assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 65537, P(16), P(16), P(16), None) == qx.QX_E_ARG
+    assert lib.qx_gemm_a8(ctypes.byref(d), None, 0, None, None, None, None) == qx.QX_OK

@@ -69,3 +69,88 @@ def test_gemv_a8_single_nonzero_activation(gpu):
         y = pw.gemv_a8(to_dev(x)).cpu().numpy()
         ref = a8.gemv_a8(q.codes, 64, q.scales, q.zeros, x)
         assert oracle.normwise_rel_err(y, ref) <= 2.0**-10, j
+
+
+# ------------------------------------------------------------ many rows: qx_gemm_a8
+def _x_rows(m, k, seed):
+    X = activations(k, seed=seed, m=m)
+    if m > 2:
+        X[1] = 0                                    # an all-zero token: xq = 0, s_x = 0
+        X[2, (seed * 7) % k] = np.float16(65504.0)  # one huge value: every other code rounds to ~0
+    return X
+
+
+@pytest.mark.parametrize("m,k", [(1, 128), (5, 384), (37, 4096), (130, 11008), (7, 1 << 14)])
+def test_quantize_a8_rows_bit_exact(gpu, m, k):
+    """qx_quantize_a8 takes each row's integer decision exactly as the oracle: int8 codes
+    and the fp32 scale bit for bit (zero row and single huge value included)."""
+    qx = gpu
+    X = _x_rows(m, k, seed=m + k)
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Xq, sx = Xq.cpu().numpy(), sx.cpu().numpy()
+    for r in range(m):
+        q, s = a8.quantize_activation(X[r])
+        assert np.array_equal(Xq[r], q), r
+        assert np.float32(sx[r]).view(np.uint32) == np.float32(s).view(np.uint32), r
+
+
+GEMM_A8 = [(1, 40, 1152), (3, 100, 384), (16, 130, 4096), (17, 64, 11008), (33, 300, 1024),
+           (64, 257, 4096), (65, 64, 2048), (512, 200, 4096)]
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=lambda f: f"b{f[0]}g{f[1]}")
+@pytest.mark.parametrize("m,n,k", GEMM_A8, ids=lambda v: str(v))
+def test_gemm_a8_matches_oracle(gpu, fmt, m, n, k):
+    """Every row of qx_gemm_a8 against the oracle's per-token A8 GEMV of that row."""
+    qx = gpu
+    bits, g = fmt
+    print(f"a8 gemm {fmt} m={m} {n}x{k}", flush=True)
+    q = realistic_quant(n, k, bits, g, 0, seed=n + k + m + bits)
+    X = _x_rows(m, k, seed=k + g + m)
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = qx.PackedWeight.from_quant(q).gemm_a8(Xq, sx).cpu().numpy()
+    for r in range(m):
+        ref = a8.gemv_a8(q.codes, g, q.scales, q.zeros, X[r])
+        if not np.any(ref):
+            assert not np.any(Y[r].astype(np.float32)), r
+            continue
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, (r, oracle.normwise_rel_err(Y[r], ref))
+
+
+@pytest.mark.parametrize("bits,g", [(3, 128), (4, 32)])
+def test_gemm_a8_integer_results_are_exact(gpu, bits, g):
+    """Scales 1, activations integers with one entry 127 per row (so inv = 1 and s_x = 1
+    exactly; that column's codes equal the zero point): every output is the integer sum
+    of (q - z) * x, small enough to be exact in binary16, bit for bit."""
+    qx = gpu
+    n, k, m = 80, 1024, 48
+    rng = np.random.default_rng(bits * g)
+    G = k // g
+    codes = rng.integers(0, 2 ** bits, (n, k), dtype=np.uint8)
+    zeros = rng.integers(0, 2 ** bits, (n, G)).astype(np.float16).view(np.uint16)
+    scales = np.ones((n, G), np.float16).view(np.uint16)
+    q = qi.QuantWeight(n, k, bits, g, 0, codes, scales=scales, zeros=zeros)
+    codes[:, 5] = zeros.view(np.float16)[:, 5 // g].astype(np.uint8)  # q - z = 0 where x = 127
+    X = rng.integers(-1, 2, (m, k)).astype(np.float16)
+    X[:, 5] = 127
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = qx.PackedWeight.from_quant(q).gemm_a8(Xq, sx).cpu().numpy()
+    d = codes.astype(np.int64) - np.repeat(zeros.view(np.float16).astype(np.int64), g, axis=1)
+    ref = X.astype(np.int64) @ d.T
+    assert np.abs(ref).max() < 2048
+    assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))
+
+
+def test_gemm_a8_rows_equal_gemv_a8_within_tolerance_and_repeat_bitwise(gpu):
+    qx = gpu
+    q = realistic_quant(500, 4096, 3, 128, 0, seed=9)
+    pw = qx.PackedWeight.from_quant(q)
+    X = activations(4096, seed=4, m=6)
+    Xd = to_dev(X)
+    Xq, sx = qx.quantize_a8(Xd)
+    Y1 = pw.gemm_a8(Xq, sx).cpu().numpy()
+    Y2 = pw.gemm_a8(Xq, sx).cpu().numpy()
+    assert np.array_equal(Y1.view(np.uint16), Y2.view(np.uint16))
+    for r in range(6):
+        y = pw.gemv_a8(Xd[r].contiguous()).cpu().numpy()
+        assert oracle.normwise_rel_err(Y1[r], y.astype(np.float64)) <= TOL
