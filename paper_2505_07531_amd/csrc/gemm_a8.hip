@@ -9,13 +9,14 @@
 // the A operand xq, and each k-step of 32 codes lies in one group (g >= 32), so a
 // group's int32 tile is scaled by its s and added to an fp32 tile when it ends.
 //
-// Work split: a block owns 64 weight rows (16 per wave: the MFMA columns) and
-// 16*MT activation rows (the MFMA rows), and walks k one 128-code chunk at a time:
-// the chunk's activation tile, codes and group words go to LDS, the next chunk's
-// are loaded into registers meanwhile. Lane group g (lane / 16) of k-step T takes
-// the 8 consecutive codes of slot 4T + g; the slots are chosen so that the four
-// lane groups decode one field kind per step (3-bit: bits 0-2, bits 3-5 or the
-// spare codes), with per-lane byte offsets and shifts.
+// Work split: a block owns 16*(4/KS) weight rows (the MFMA columns; 16 per group of
+// KS waves) and 16*MT activation rows (the MFMA rows), and walks k KS chunks at a
+// time, wave ks of a group taking chunk ks: the chunks' activation tiles, codes and
+// group words go to LDS, the next ones are loaded into registers meanwhile, and the
+// KS partial tiles are added through LDS at the end. Lane group g (lane / 16) of
+// k-step T takes the 8 consecutive codes of slot 4T + g; the slots are chosen so
+// that the four lane groups decode one field kind per step (3-bit: bits 0-2, bits
+// 3-5 or the spare codes), with per-lane byte offsets and shifts.
 #include "qx_device.h"
 #include "qx_internal.h"
 
@@ -106,52 +107,58 @@ __device__ __forceinline__ u32x2 slot_codes(const char* cb, int g) {
   }
 }
 
-template <int BITS, int G, int MT>
+template <int BITS, int G, int MT, int KS>
 __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restrict__ packed,
                                                              const int8_t* __restrict__ Xq,
                                                              const float* __restrict__ sx,
                                                              uint16_t* __restrict__ Y, int n, int k,
                                                              int m) {
-  constexpr int BM = 16 * MT, BN = 64, NG = 128 / G;
+  constexpr int NW = 4 / KS;                // wave groups on different weight rows
+  constexpr int BM = 16 * MT, BN = 16 * NW, NG = 128 / G;
   constexpr int CS = 80;        // LDS bytes per weight row of the code tile (bank-spread rows)
   constexpr int XS = 144;       // LDS bytes per activation row of the activation tile
-  constexpr int XPC = BM * 8;   // 16-byte activation pieces per chunk
+  constexpr int XPC = KS * BM * 8;   // 16-byte activation pieces per step (KS chunks)
   constexpr int XP = (XPC + kA8Threads - 1) / kA8Threads;
-  constexpr int CPC = BN * BITS;  // 16-byte code pieces per chunk
+  constexpr int CPC = KS * BN * BITS;  // 16-byte code pieces per step
   constexpr int CP = (CPC + kA8Threads - 1) / kA8Threads;
-  constexpr int MPC = BN * NG;  // group words per chunk
+  constexpr int MPC = KS * BN * NG;  // group words per step
   constexpr int MP = (MPC + kA8Threads - 1) / kA8Threads;
-  __shared__ __align__(16) char xs[BM * XS];
-  __shared__ __align__(16) char cs[BN * CS];
-  __shared__ uint32_t ms[BN * NG];
+  static_assert((KS - 1) * NW * MT * 1024 <= KS * BM * XS, "the k-split reduction must fit the LDS tile");
+  __shared__ __align__(16) char xs[KS * BM * XS];
+  __shared__ __align__(16) char cs[KS * BN * CS];
+  __shared__ uint32_t ms[KS * BN * NG];
 
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
   const int C = k >> 7, G_row = k / G;
   const size_t meta_off = (size_t)n * k * BITS / 8;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63, g = lane >> 4, li = lane & 15;
+  const int ks = wave % KS, wr = wave / KS;  // this wave's chunk within a step, weight-row group
 
-  // chunk c of the tiles into registers (rows clamped in bounds; clamped copies are
-  // never stored to Y)
+  // chunks c0 .. c0 + KS - 1 of the tiles into registers (rows and chunks clamped in
+  // bounds; clamped copies are never multiplied or stored)
   u32x4 xr[XP], cr[CP];
   uint32_t mr[MP];
-  auto load = [&](int c) {
+  auto load = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < XP; ++i) {
       const int p = min(t + i * kA8Threads, XPC - 1);
-      const int row = min(m0 + (p >> 3), m - 1);
-      xr[i] = *reinterpret_cast<const u32x4*>(Xq + (size_t)row * k + (size_t)c * 128 + (p & 7) * 16);
+      const int q = p / (BM * 8), pr = p % (BM * 8);
+      const int row = min(m0 + (pr >> 3), m - 1), c = min(c0 + q, C - 1);
+      xr[i] = *reinterpret_cast<const u32x4*>(Xq + (size_t)row * k + (size_t)c * 128 + (pr & 7) * 16);
     }
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
       const int p = min(t + i * kA8Threads, CPC - 1);
-      const int row = min(n0 + p / BITS, n - 1), sl = p % BITS;
+      const int q = p / (BN * BITS), pr = p % (BN * BITS);
+      const int row = min(n0 + pr / BITS, n - 1), sl = pr % BITS, c = min(c0 + q, C - 1);
       cr[i] = *reinterpret_cast<const u32x4*>(packed + (((size_t)row * BITS + sl) * C + c) * 16);
     }
 #pragma unroll
     for (int i = 0; i < MP; ++i) {
       const int p = min(t + i * kA8Threads, MPC - 1);
-      const int row = min(n0 + p / NG, n - 1);
-      mr[i] = *reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + c * NG + p % NG) * 4);
+      const int q = p / (BN * NG), pr = p % (BN * NG);
+      const int row = min(n0 + pr / NG, n - 1), c = min(c0 + q, C - 1);
+      mr[i] = *reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + c * NG + pr % NG) * 4);
     }
   };
   auto store = [&]() {
@@ -182,10 +189,13 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
   load(0);
   store();
   __syncthreads();
-  const char* crow = cs + (16 * wave + li) * CS;  // this lane's weight row (MFMA column li)
-  const uint32_t* mrow = ms + (16 * wave + li) * NG;
-  for (int c = 0; c < C; ++c) {
-    if (c + 1 < C) load(c + 1);
+  // this wave's tiles: activation rows of chunk ks, weight row (MFMA column) li of group wr
+  const char* xw = xs + ks * BM * XS;
+  const char* crow = cs + (ks * BN + 16 * wr + li) * CS;
+  const uint32_t* mrow = ms + (ks * BN + 16 * wr + li) * NG;
+  for (int c0 = 0; c0 < C; c0 += KS) {
+    if (c0 + KS < C) load(c0 + KS);
+    if (c0 + ks < C) {
 #define QX_A8_KSTEP(T)                                                                          \
   {                                                                                             \
     constexpr int grp = (32 * (T)) / G;                                                         \
@@ -195,7 +205,7 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
     const u32x2 q = slot_codes<BITS, T>(crow, g);                                               \
     const long b = (long)(((uint64_t)minus_z(q.y, zz) << 32) | minus_z(q.x, zz));               \
     _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                         \
-      const long a = *reinterpret_cast<const long*>(xs + (16 * mt + li) * XS + 32 * (T) + 8 * g); \
+      const long a = *reinterpret_cast<const long*>(xw + (16 * mt + li) * XS + 32 * (T) + 8 * g); \
       part[mt] = __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, part[mt], 0, 0, 0);                \
     }                                                                                           \
     if constexpr ((32 * ((T) + 1)) % G == 0) { /* the group ends: scale and add */              \
@@ -206,20 +216,38 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
       }                                                                                         \
     }                                                                                           \
   }
-    QX_A8_KSTEP(0)
-    QX_A8_KSTEP(1)
-    QX_A8_KSTEP(2)
-    QX_A8_KSTEP(3)
+      QX_A8_KSTEP(0)
+      QX_A8_KSTEP(1)
+      QX_A8_KSTEP(2)
+      QX_A8_KSTEP(3)
 #undef QX_A8_KSTEP
-    __syncthreads();  // every wave is done with chunk c
-    if (c + 1 < C) {
+    }
+    __syncthreads();  // every wave is done with these chunks
+    if (c0 + KS < C) {
       store();
       __syncthreads();
     }
   }
 
+  // KS partial tiles -> one, in ks order, through LDS (every wave passed the last barrier)
+  if constexpr (KS > 1) {
+    float* red = reinterpret_cast<float*>(xs);
+    if (ks > 0) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        *reinterpret_cast<f4_t*>(red + (((ks - 1) * NW + wr) * MT + mt) * 256 + 4 * lane) = acc[mt];
+    }
+    __syncthreads();
+    if (ks > 0) return;
+#pragma unroll
+    for (int q = 1; q < KS; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] += *reinterpret_cast<const f4_t*>(red + (((q - 1) * NW + wr) * MT + mt) * 256 + 4 * lane);
+  }
+
   // D of a 16x16 tile: lane holds activation rows 4g + r, weight row (column) li
-  const int col = n0 + 16 * wave + li;
+  const int col = n0 + 16 * wr + li;
   if (col < n) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -231,20 +259,23 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
   }
 }
 
+template <int BITS, int G, int MT, int KS>
+void launch_a8_cfg(const qx_desc* d, const char* p, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
+                   hipStream_t s) {
+  constexpr int BN = 16 * (4 / KS), BM = 16 * MT;
+  const dim3 grid((unsigned)((d->n + BN - 1) / BN), (unsigned)((m + BM - 1) / BM));
+  hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, MT, KS>), grid, dim3(kA8Threads), 0, s, p, Xq, sx, Y, d->n, d->k, m);
+}
+
+// Tiles by m: few activation rows split each weight tile's chunks over the four
+// waves (more blocks, k-split partials added through LDS); many rows give each
+// wave 64 activation rows so that each decoded code feeds four MFMAs.
 template <int BITS, int G>
 int launch_gemm_a8_t(const qx_desc* d, const char* p, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
                      hipStream_t s) {
-  const unsigned nx = (unsigned)((d->n + 63) / 64);
-  if (m <= 16) {
-    hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, 1>), dim3(nx, (unsigned)((m + 15) / 16)), dim3(kA8Threads), 0, s,
-                       p, Xq, sx, Y, d->n, d->k, m);
-  } else if (m <= 32) {
-    hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, 2>), dim3(nx, (unsigned)((m + 31) / 32)), dim3(kA8Threads), 0, s,
-                       p, Xq, sx, Y, d->n, d->k, m);
-  } else {
-    hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, 4>), dim3(nx, (unsigned)((m + 63) / 64)), dim3(kA8Threads), 0, s,
-                       p, Xq, sx, Y, d->n, d->k, m);
-  }
+  if (m <= 16) launch_a8_cfg<BITS, G, 1, 4>(d, p, m, Xq, sx, Y, s);
+  else if (m <= 64) launch_a8_cfg<BITS, G, 2, 2>(d, p, m, Xq, sx, Y, s);
+  else launch_a8_cfg<BITS, G, 4, 1>(d, p, m, Xq, sx, Y, s);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 
