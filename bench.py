@@ -542,6 +542,10 @@ def main():
             log(f"cpu baseline in {time.time() - t0:.0f}s")
         else:
             out["cpu_baseline"] = None
+        props = torch.cuda.get_device_properties(0)
+        out["device"] = {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
+                         "compute_units": props.multi_processor_count,
+                         "memory_gb": round(props.total_memory / 1e9, 1)}
         print(json.dumps(out), flush=True)
     elif args.workload == "counters":
         print(json.dumps(bench_kernel_counters(args, qx)), flush=True)

@@ -19,9 +19,27 @@ namespace {
 // Uniform pairs are "M + q" (the zero point is folded per group by the caller).
 template <int BITS, int KIND, int G, typename F>
 __device__ __forceinline__ void for_each_pair(const Item<BITS, KIND, G>& it, const DecodeConsts& k,
-                                              F&& emit) {
+                                              const uint32_t* q4lut, F&& emit) {
   constexpr int NG = 128 / G;
-  if constexpr (BITS == 4 && KIND == QX_UNIFORM) {
+  if constexpr (KIND == QX_Q4X) {  // two groups of 64: the selected sub-codebook's tables
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const uint32_t* tp = q4lut + 8 * ((it.m[1] >> (2 * g)) & 3u);
+      const u32x4 tl = *reinterpret_cast<const u32x4*>(tp), th = *reinterpret_cast<const u32x4*>(tp + 4);
+      const LutGroup<4> t = {{tl.x, tl.y, tl.z, tl.w}, {th.x, th.y, th.z, th.w}};
+#pragma unroll
+      for (int j = 8 * g; j < 8 * g + 8; ++j) {
+        const uint32_t D = it.d[j];
+        uint32_t elo, ehi, olo, ohi;
+        lut4_bytes(t, D & 0x0F0F0F0Fu, elo, ehi);
+        lut4_bytes(t, (D >> 4) & 0x0F0F0F0Fu, olo, ohi);
+        emit(g, perm(ehi, elo, 0x06020400u), 4 * j);
+        emit(g, perm(ohi, olo, 0x06020400u), 4 * j + 1);
+        emit(g, perm(ehi, elo, 0x07030501u), 4 * j + 2);
+        emit(g, perm(ohi, olo, 0x07030501u), 4 * j + 3);
+      }
+    }
+  } else if constexpr (BITS == 4 && KIND == QX_UNIFORM) {
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int g = (8 * j) / G;
@@ -125,6 +143,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
                                                           uint16_t* __restrict__ Y, int n, int k,
                                                           int m, int R, int S) {
   extern __shared__ __align__(16) char smem[];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   constexpr int NG = 128 / G;
   const int C = k >> 7, G_row = k / G, nthreads = blockDim.x;
   const size_t meta_off = (size_t)n * k * BITS / 8;
@@ -151,6 +170,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
     }
     load_item<BITS, KIND, G>(it, packed, meta_off, row, seg * S + min(c, cs - 1), C, G_row);
   };
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);  // read after the first barrier
   float tot[M];
 #pragma unroll
   for (int v = 0; v < M; ++v) tot[v] = 0.f;
@@ -173,7 +193,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
     for (int v = 0; v < M; ++v)
 #pragma unroll
       for (int g = 0; g < NG; ++g) acc[v][g] = 0.f;
-    for_each_pair<BITS, KIND, G>(cur, kc, [&](int g, uint32_t pair, int xdw) {
+    for_each_pair<BITS, KIND, G>(cur, kc, q4lut, [&](int g, uint32_t pair, int xdw) {
 #pragma unroll
       for (int v = 0; v < M; ++v)
         acc[v][g] = dot2(pair, reinterpret_cast<const uint32_t*>(xb + v * xbytes)[xdw], acc[v][g]);
@@ -184,6 +204,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
           if constexpr (KIND == QX_UNIFORM) tot[v] += fold_group(cur.m[g], acc[v][g], gs[v * S * NG + c * NG + g]);
+          else if constexpr (KIND == QX_Q4X) tot[v] += half_bits_to_float((cur.m[0] >> (16 * g)) & 0xFFFFu) * acc[v][g];
           else tot[v] += acc[v][g];
         }
       }
@@ -252,9 +273,10 @@ int launch_multi_t(const qx_desc* d, const void* packed, int m, const uint16_t* 
 // each with a long k loop); at m = 3, 4 with k <= n the GEMM is as fast or faster.
 // 4-bit codebooks of 32-code groups (a 32-byte table per 32 codes) decode faster
 // into matrix-core fragments at every m; at m = 2 so do 4-bit 64-code groups when
-// k <= n.
+// k <= n. Q4X (whose 16-entry lookups make the GEMM decode-bound) runs GEMV-style
+// for every m <= 4.
 bool gemv_multi_applies(const qx_desc* d, int m) {
-  if (d->kind == QX_Q4X) return m == 1;  // the small-batch kernel has no Q4X path
+  if (d->kind == QX_Q4X) return m >= 1 && m <= QX_MULTI_MAX_M;
   if (m < 1 || m > QX_MULTI_MAX_M) return false;
   const bool cb4 = d->kind == QX_CODEBOOK && d->bits == 4;
   if (cb4 && d->group == 32) return false;
@@ -270,6 +292,7 @@ int launch_gemv_multi(const qx_desc* d, const void* packed, int m, const uint16_
   QX_MULTI_CASE(3, 1, 32) QX_MULTI_CASE(3, 1, 64) QX_MULTI_CASE(3, 1, 128)
   QX_MULTI_CASE(4, 0, 32) QX_MULTI_CASE(4, 0, 64) QX_MULTI_CASE(4, 0, 128)
   QX_MULTI_CASE(4, 1, 32) QX_MULTI_CASE(4, 1, 64) QX_MULTI_CASE(4, 1, 128)
+  QX_MULTI_CASE(4, 2, 64)
 #undef QX_MULTI_CASE
   return QX_E_UNSUPPORTED;
 }

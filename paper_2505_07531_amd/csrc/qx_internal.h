@@ -42,7 +42,7 @@ int launch_gemm_a8(const qx_desc* d, const void* packed, int m, const int8_t* Xq
                    hipStream_t s);
 
 // Products of at most QX_MULTI_MAX_M rows may run GEMV-style (gemv_multi_applies
-// decides; launch_gemv_multi takes 2 <= m <= QX_MULTI_MAX_M, any k, not Q4X).
+// decides; launch_gemv_multi takes 2 <= m <= QX_MULTI_MAX_M, any k, every kind).
 #ifndef QX_MULTI_MAX_M
 #define QX_MULTI_MAX_M 4
 #endif

@@ -122,17 +122,19 @@ def test_q4x_max_k(gpu):
     assert oracle.normwise_rel_err(pw.gemv(to_dev(x)).cpu().numpy(), oracle.gemv(w16, x)) <= TOL
 
 
-GEMM_CASES = [(1, 40, 1152), (2, 40, 1152), (3, 130, 4096), (16, 100, 384), (17, 37, 11008),
-              (64, 300, 1024), (65, 64, 4096), (512, 260, 2048)]
+GEMM_CASES = [(1, 40, 1152), (2, 40, 1152), (3, 130, 4096), (4, 4096, 4096), (2, 11008, 4096),
+              (4, 300, 11008), (16, 100, 384), (17, 37, 11008), (64, 300, 1024), (65, 64, 4096),
+              (512, 260, 2048)]
 
 
 @pytest.mark.parametrize("m,n,k", GEMM_CASES, ids=lambda v: str(v))
 def test_q4x_gemm_matches_oracle(gpu, m, n, k):
-    """qx_gemm on Q4X (m = 1: the GEMV; else the matrix-core GEMM with W' decoded into
-    its operands as fp16(s * CB[t][q])): every output row within the parity bound."""
+    """qx_gemm on Q4X (m = 1: the GEMV; m = 2-4: the small-batch kernel; else the
+    matrix-core GEMM with W' decoded into its operands as fp16(s * CB[t][q])): every
+    output row within the parity bound."""
     qx = gpu
     print(f"q4x gemm m={m} {n}x{k}", flush=True)
-    q = random_q4x(n, k, seed=m * 7 + n) if m % 2 else realistic_q4x(n, k, seed=m + n)
+    q = random_q4x(n, k, seed=m * 7 + n) if m % 2 or n * k > 10**7 else realistic_q4x(n, k, seed=m + n)
     X = activations(k, seed=m + 3, m=m)
     Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
     w = _ref(q)
