@@ -171,6 +171,19 @@ def test_gemm_small_batch(gpu, fmt, m, shape):
         assert oracle.normwise_rel_err(Y[r][rows], ref) <= TOL, r
 
 
+@pytest.mark.parametrize("m", [2, 4])
+def test_gemm_small_batch_longest_k(gpu, m):
+    """k = 2^20 (8192 chunks, 256 segments of the small-batch kernel), rows of the oracle."""
+    qx = gpu
+    n, k = 5, 1 << 20
+    q = random_quant(n, k, 4, 128, 0, seed=m)
+    X = activations(k, seed=m + 11, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    w16 = _ref_w16(q)
+    for r in range(m):
+        assert oracle.normwise_rel_err(Y[r], oracle.gemv(w16, X[r])) <= TOL, r
+
+
 def test_gemm_one_row_is_the_gemv(gpu):
     """m = 1 runs the batch-1 GEMV: the same bits as qx_gemv."""
     qx = gpu
