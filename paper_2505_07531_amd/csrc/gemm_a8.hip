@@ -269,12 +269,17 @@ void launch_a8_cfg(const qx_desc* d, const char* p, int m, const int8_t* Xq, con
 
 // Tiles by m: few activation rows split each weight tile's chunks over the four
 // waves (more blocks, k-split partials added through LDS); many rows give each
-// wave 64 activation rows so that each decoded code feeds four MFMAs.
+// wave 64 activation rows so that each decoded code feeds four MFMAs, and still
+// split k when 64 x 64 tiles would leave fewer than 512 blocks (e.g. 4096 weight
+// rows at m = 128: 128 blocks with the whole k, 512 with it split four ways).
 template <int BITS, int G>
 int launch_gemm_a8_t(const qx_desc* d, const char* p, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
                      hipStream_t s) {
+  const long tiles64 = (long)((d->n + 63) / 64) * ((m + 63) / 64);
   if (m <= 16) launch_a8_cfg<BITS, G, 1, 4>(d, p, m, Xq, sx, Y, s);
   else if (m <= 64) launch_a8_cfg<BITS, G, 2, 2>(d, p, m, Xq, sx, Y, s);
+  else if (tiles64 < 256) launch_a8_cfg<BITS, G, 4, 4>(d, p, m, Xq, sx, Y, s);
+  else if (tiles64 < 512) launch_a8_cfg<BITS, G, 4, 2>(d, p, m, Xq, sx, Y, s);
   else launch_a8_cfg<BITS, G, 4, 1>(d, p, m, Xq, sx, Y, s);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }

@@ -95,7 +95,8 @@ def test_quantize_a8_rows_bit_exact(gpu, m, k):
 
 
 GEMM_A8 = [(1, 40, 1152), (3, 100, 384), (16, 130, 4096), (17, 64, 11008), (33, 300, 1024),
-           (64, 257, 4096), (65, 64, 2048), (512, 200, 4096), (3, 9, 1 << 18)]
+           (64, 257, 4096), (65, 64, 2048), (512, 200, 4096), (3, 9, 1 << 18), (256, 4096, 512),
+           (130, 2000, 1024)]
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=lambda f: f"b{f[0]}g{f[1]}")
