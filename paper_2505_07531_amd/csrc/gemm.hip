@@ -469,7 +469,9 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16
 }
 
 // Tile shape per activation row count (from a sweep of MT, NT, KS, S, DX on the
-// 3-bit g64 MLP shapes at m = 16, 64, 512). Small m is bound by streaming the codes:
+// 3-bit g64 MLP shapes at m = 16, 64, 512, and for uniform codes at m = 128-512 a
+// split of k when the 128 x 64 tiles are few: 4096x11008 at m = 128 took 113 us
+// whole and 57 us split four ways). Small m is bound by streaming the codes:
 // one 16-row activation tile, 16 weight rows per block and the chunks of a row
 // split over the four waves, so that the grid has enough blocks. Larger m gets
 // larger activation tiles so that each decoded weight feeds more MFMAs; with
@@ -493,8 +495,15 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint
       else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
       break;
     default:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2>(d, p, m, X, Y, s);
-      else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
+      if constexpr (kUni) {
+        // few 128 x 64 tiles (e.g. 4096 weight rows at m <= 256): split k over the waves
+        const long tiles = (long)((d->n + 127) / 128) * ((m + 63) / 64);
+        if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1>(d, p, m, X, Y, s);
+        else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2>(d, p, m, X, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2>(d, p, m, X, Y, s);
+      } else {
+        launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
+      }
       break;
   }
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
