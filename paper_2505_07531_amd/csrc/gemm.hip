@@ -469,9 +469,9 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16
 }
 
 // Tile shape per activation row count (from a sweep of MT, NT, KS, S, DX on the
-// 3-bit g64 MLP shapes at m = 16, 64, 512, and for uniform codes at m = 128-512 a
-// split of k when the 128 x 64 tiles are few: 4096x11008 at m = 128 took 113 us
-// whole and 57 us split four ways). Small m is bound by streaming the codes:
+// 3-bit g64 MLP shapes at m = 16, 64, 512, and at m = 128-512 a split of k when
+// the tiles are few: uniform 4096x11008 at m = 128 took 113 us whole and 57 us
+// split four ways, codebook-3 78 and 55 us split two ways). Small m is bound by streaming the codes:
 // one 16-row activation tile, 16 weight rows per block and the chunks of a row
 // split over the four waves, so that the grid has enough blocks. Larger m gets
 // larger activation tiles so that each decoded weight feeds more MFMAs; with
@@ -502,7 +502,10 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint
         else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2>(d, p, m, X, Y, s);
         else launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2>(d, p, m, X, Y, s);
       } else {
-        launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
+        // codebook and Q4X: 64 x 64 tiles; at most 128 of them split k over two waves
+        const long tiles = (long)((d->n + 63) / 64) * ((m + 63) / 64);
+        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 1, 2, 4, 2>(d, p, m, X, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
       }
       break;
   }

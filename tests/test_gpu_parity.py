@@ -215,7 +215,8 @@ def test_gemm_prefill_shapes(gpu, m, name):
 
 # activation tiles mapped to XCDs with padding blocks, single-chunk rows, chunk counts
 # that leave K-split waves idle in the last round
-GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40), (1, 640, 17)]
+GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40), (1, 640, 17),
+              (4096, 1152, 128), (2000, 1536, 200)]
 
 
 @pytest.mark.parametrize("fmt", [(3, 0, 64), (4, 0, 128), (3, 1, 32), (4, 1, 32)], ids=_fmt_id)
