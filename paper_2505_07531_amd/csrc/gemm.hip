@@ -471,7 +471,8 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16
 // Tile shape per activation row count (from a sweep of MT, NT, KS, S, DX on the
 // 3-bit g64 MLP shapes at m = 16, 64, 512, and at m = 128-512 a split of k when
 // the tiles are few: uniform 4096x11008 at m = 128 took 113 us whole and 57 us
-// split four ways, codebook-3 78 and 55 us split two ways). Small m is bound by streaming the codes:
+// split four ways, codebook-3 78 and 55 us split two ways; at m = 32, 35 and 27 us
+// with four waves instead of two on each 32 x 32 tile). Small m is bound by streaming the codes:
 // one 16-row activation tile, 16 weight rows per block and the chunks of a row
 // split over the four waves, so that the grid has enough blocks. Larger m gets
 // larger activation tiles so that each decoded weight feeds more MFMAs; with
@@ -491,8 +492,14 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint
       else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1>(d, p, m, X, Y, s);
       break;
     case 2:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1>(d, p, m, X, Y, s);
-      else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
+      if constexpr (kUni) {
+        // at most 128 tiles of 32 x 32 (a 4096-row matrix at m <= 32): four waves per tile
+        const long tiles = (long)((d->n + 31) / 32) * ((m + 31) / 32);
+        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 1>(d, p, m, X, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1>(d, p, m, X, Y, s);
+      } else {
+        launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
+      }
       break;
     default:
       if constexpr (kUni) {

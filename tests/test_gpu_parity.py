@@ -195,10 +195,10 @@ def test_gemm_one_row_is_the_gemv(gpu):
     assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
 
 
-@pytest.mark.parametrize("m", [16, 64, 128, 256, 512])
+@pytest.mark.parametrize("m", [16, 32, 64, 128, 256, 512])
 @pytest.mark.parametrize("name", ["gate", "down"])
 def test_gemm_prefill_shapes(gpu, m, name):
-    """c5 matrices; down at m = 128 / 256 takes the k split over four / two waves."""
+    """c5 matrices; down at m = 32 / 128 / 256 takes the k split over more waves."""
     qx = gpu
     spec = configs.c5_matrix(name)
     print(f"gemm c5 {name} m={m}", flush=True)
