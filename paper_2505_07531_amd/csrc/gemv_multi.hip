@@ -1,12 +1,13 @@
-// Small-batch decode: Y = X W'^T for m <= 4 activation rows, GEMV-style. Every
+// Small-batch decode: Y = X W'^T for 2 to 4 activation rows, GEMV-style. Every
 // code is decoded once per lane (as in the batch-1 GEMV) and its weight pairs are
 // multiplied with each of the m activation vectors staged in LDS, so the decode
-// work is shared by the batch and the matrix is still streamed once; for m this
-// small the matrix-core GEMM, whose blocks synchronise for every round of chunks,
-// leaves the memory system idle most of the time. A block takes R rows and walks
-// the reduction axis in segments of S 128-code chunks (one item per lane and
-// segment), so the LDS it needs does not grow with k; lane totals go through LDS
-// and one wave per (row, vector) adds them in a fixed order.
+// work is shared by the batch and the matrix is still streamed once, where the
+// matrix-core GEMM would multiply 16-row activation tiles that are mostly padding
+// (gemv_multi_applies picks between the two per shape and format, from
+// measurements). A block takes R rows and walks the reduction axis in segments of
+// S 128-code chunks (one item per lane and segment), so the LDS it needs does not
+// grow with k; lane totals go through LDS and one wave per (row, vector) adds them
+// in a fixed order.
 #include "gemv_common.h"
 
 #include <algorithm>
