@@ -69,6 +69,23 @@ __device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, ui
   return perm(perm(d, c, 0x04000C0Cu), perm(b, a, 0x0C0C0400u), 0x07060100u);
 }
 
+// One piece of int8 activations (8 values, decoder order) to LDS, and the sum of
+// xq over each group, whose pieces sit in consecutive lanes (every lane calls this).
+template <int G>
+__device__ __forceinline__ void store_x8(u32x2 o, int p, int C, char* xs, float* gs) {
+  const bool valid = p < C * 16;
+  if (valid) *reinterpret_cast<u32x2*>(xs + (p >> 4) * kX8Block + (p & 15) * 8) = o;
+  constexpr int PPG = G / 8;  // pieces per group, consecutive lanes
+  float s = (float)__builtin_amdgcn_sdot4((int)o.y, 0x01010101, __builtin_amdgcn_sdot4((int)o.x, 0x01010101, 0, false), false);
+  if constexpr (PPG >= 4) {
+    s = dpp_plus<0xB1, 0xF>(s);
+    s = dpp_plus<0x4E, 0xF>(s);
+    if constexpr (PPG >= 8) s = dpp_plus<0x141, 0xF>(s);
+    if constexpr (PPG >= 16) s = dpp_plus<0x140, 0xF>(s);
+  }
+  if (valid && (p & (PPG - 1)) == 0) gs[p / PPG] = s;
+}
+
 // Quantize the staged pieces of x (XP 16-byte pieces per thread, piece p = chunk
 // p/16, values 8*(p%16)..) with the block-wide scale, store them in LDS as int8 in
 // the order the decoder consumes them (b = 4: per 8 codes the even then the odd
@@ -112,19 +129,22 @@ __device__ __forceinline__ float stage_x_a8(const u32x4 (&xr)[XP], int C, char* 
       o.x = pack4(q[0], q[1], q[2], q[3]);
       o.y = pack4(q[4], q[5], q[6], q[7]);
     }
-    const bool valid = p < C * 16;
-    if (valid) *reinterpret_cast<u32x2*>(xs + (p >> 4) * kX8Block + (p & 15) * 8) = o;
-    constexpr int PPG = G / 8;  // pieces per group, consecutive lanes
-    float s = (float)__builtin_amdgcn_sdot4((int)o.y, 0x01010101, __builtin_amdgcn_sdot4((int)o.x, 0x01010101, 0, false), false);
-    if constexpr (PPG >= 4) {
-      s = dpp_plus<0xB1, 0xF>(s);
-      s = dpp_plus<0x4E, 0xF>(s);
-      if constexpr (PPG >= 8) s = dpp_plus<0x141, 0xF>(s);
-      if constexpr (PPG >= 16) s = dpp_plus<0x140, 0xF>(s);
-    }
-    if (valid && (p & (PPG - 1)) == 0) gs[p / PPG] = s;
+    store_x8<G>(o, p, C, xs, gs);
   }
   return amax > 0.f ? amax / 127.f : 0.f;
+}
+
+// Stage int8 activations already quantized (qx_quantize_a8: natural order, 8 bytes
+// per piece) like stage_x_a8 stages its own: decoder order, group sums of xq.
+template <int BITS, int G, int XP>
+__device__ __forceinline__ void stage_xq_a8(const u32x2 (&xr)[XP], int C, char* xs, float* gs, int nthreads) {
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    const int p = threadIdx.x + i * nthreads;
+    u32x2 o = xr[i];
+    if constexpr (BITS == 4) o = u32x2{perm(xr[i].y, xr[i].x, 0x06040200u), perm(xr[i].y, xr[i].x, 0x07050301u)};
+    store_x8<G>(o, p, C, xs, gs);
+  }
 }
 
 // sum_j s_j * (sum q*xq - z_j * sum xq) over the groups of one chunk.
@@ -179,9 +199,11 @@ __device__ __forceinline__ float chunk_dot_a8(const CodesA8<BITS, G>& it, const 
 }
 
 // k = 128*LPR with LPR in {32, 64}: as the fp16 wave kernel.
-template <int BITS, int G, int LPR, int WPB>
+// PREQ: x is already int8 (qx_quantize_a8) with its scale at *sxp; else fp16.
+template <int BITS, int G, int LPR, int WPB, bool PREQ>
 __global__ __launch_bounds__(64 * WPB) void gemv_a8_wave_kernel(const char* __restrict__ packed,
-                                                                const uint16_t* __restrict__ x,
+                                                                const void* __restrict__ x,
+                                                                const float* __restrict__ sxp,
                                                                 uint16_t* __restrict__ y, int n) {
   constexpr int C = LPR, NT = 64 * WPB, RPW = 64 / LPR, RPB = WPB * RPW;
   constexpr int XP = (C * 16 + NT - 1) / NT;
@@ -194,13 +216,24 @@ __global__ __launch_bounds__(64 * WPB) void gemv_a8_wave_kernel(const char* __re
   const int c = lane & (LPR - 1);
   const int row = blockIdx.x * RPB + wave * RPW + lane / LPR;
 
-  u32x4 xr[XP];
-  const u32x4* src = reinterpret_cast<const u32x4*>(x);
-#pragma unroll
-  for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * NT, C * 16 - 1)];
+  float sx;
   CodesA8<BITS, G> it;
-  load_codes_a8<BITS, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
-  const float sx = stage_x_a8<BITS, G, XP>(xr, C, xs, gs, red, NT);
+  if constexpr (PREQ) {
+    u32x2 xr[XP];
+    const u32x2* src = reinterpret_cast<const u32x2*>(x);
+#pragma unroll
+    for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * NT, C * 16 - 1)];
+    load_codes_a8<BITS, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
+    stage_xq_a8<BITS, G, XP>(xr, C, xs, gs, NT);
+    sx = *sxp;
+  } else {
+    u32x4 xr[XP];
+    const u32x4* src = reinterpret_cast<const u32x4*>(x);
+#pragma unroll
+    for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * NT, C * 16 - 1)];
+    load_codes_a8<BITS, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
+    sx = stage_x_a8<BITS, G, XP>(xr, C, xs, gs, red, NT);
+  }
   __syncthreads();
   float v = chunk_dot_a8<BITS, G>(it, xs + c * kX8Block, gs + c * (128 / G));
   v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
@@ -209,9 +242,10 @@ __global__ __launch_bounds__(64 * WPB) void gemv_a8_wave_kernel(const char* __re
 
 // Any k up to 88 chunks: one (row, chunk) item per lane, R rows per block, partials
 // through LDS and one wave per row adding them in a fixed order (as the fp16 row kernel).
-template <int BITS, int G, int XP>
+template <int BITS, int G, int XP, bool PREQ>
 __global__ __launch_bounds__(1024) void gemv_a8_row_kernel(const char* __restrict__ packed,
-                                                           const uint16_t* __restrict__ x,
+                                                           const void* __restrict__ x,
+                                                           const float* __restrict__ sxp,
                                                            uint16_t* __restrict__ y, int n, int k, int R) {
   extern __shared__ __align__(16) char smem[];
   __shared__ float red[16];
@@ -222,15 +256,26 @@ __global__ __launch_bounds__(1024) void gemv_a8_row_kernel(const char* __restric
   char* xs = smem;                                                   // C * kX8Block
   float* part = reinterpret_cast<float*>(smem + C * kX8Block);       // R * C
   float* gs = part + R * C;                                          // C * 128/G
-  u32x4 xr[XP];
-  const u32x4* src = reinterpret_cast<const u32x4*>(x);
-#pragma unroll
-  for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * nthreads, C * 16 - 1)];
   const int t = threadIdx.x, r = t / C, c = t - r * C;
   const bool valid = r < rows;
+  float sx;
   CodesA8<BITS, G> it;
-  load_codes_a8<BITS, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
-  const float sx = stage_x_a8<BITS, G, XP>(xr, C, xs, gs, red, nthreads);
+  if constexpr (PREQ) {
+    u32x2 xr[XP];
+    const u32x2* src = reinterpret_cast<const u32x2*>(x);
+#pragma unroll
+    for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * nthreads, C * 16 - 1)];
+    load_codes_a8<BITS, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+    stage_xq_a8<BITS, G, XP>(xr, C, xs, gs, nthreads);
+    sx = *sxp;
+  } else {
+    u32x4 xr[XP];
+    const u32x4* src = reinterpret_cast<const u32x4*>(x);
+#pragma unroll
+    for (int i = 0; i < XP; ++i) xr[i] = src[min((int)threadIdx.x + i * nthreads, C * 16 - 1)];
+    load_codes_a8<BITS, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+    sx = stage_x_a8<BITS, G, XP>(xr, C, xs, gs, red, nthreads);
+  }
   __syncthreads();
   if (valid) part[t] = chunk_dot_a8<BITS, G>(it, xs + c * kX8Block, gs + c * (128 / G));
   __syncthreads();
@@ -260,8 +305,9 @@ void a8_row_shape(int C, int* R, int* threads) {
   *threads = 64 * ((best_r * C + 63) / 64);
 }
 
-template <int BITS, int G>
-int launch_gemv_a8_t(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
+template <int BITS, int G, bool PREQ>
+int launch_gemv_a8_t(const qx_desc* d, const void* packed, const void* x, const float* sx, uint16_t* y,
+                     hipStream_t s) {
   const char* p = static_cast<const char*>(packed);
   const int C = d->k / 128;
   constexpr int WPB = 4;
@@ -269,9 +315,9 @@ int launch_gemv_a8_t(const qx_desc* d, const void* packed, const uint16_t* x, ui
     const int rpb = WPB * 64 / C;
     const dim3 grid((unsigned)((d->n + rpb - 1) / rpb)), block(64 * WPB);
     if (C == 32)
-      hipLaunchKernelGGL((gemv_a8_wave_kernel<BITS, G, 32, WPB>), grid, block, 0, s, p, x, y, d->n);
+      hipLaunchKernelGGL((gemv_a8_wave_kernel<BITS, G, 32, WPB, PREQ>), grid, block, 0, s, p, x, sx, y, d->n);
     else
-      hipLaunchKernelGGL((gemv_a8_wave_kernel<BITS, G, 64, WPB>), grid, block, 0, s, p, x, y, d->n);
+      hipLaunchKernelGGL((gemv_a8_wave_kernel<BITS, G, 64, WPB, PREQ>), grid, block, 0, s, p, x, sx, y, d->n);
   } else if (C <= 88) {
     int R, threads;
     a8_row_shape(C, &R, &threads);
@@ -279,11 +325,11 @@ int launch_gemv_a8_t(const qx_desc* d, const void* packed, const uint16_t* x, ui
     const int xp = (C * 16 + threads - 1) / threads;
     const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
     if (xp <= 1)
-      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 1>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 1, PREQ>), grid, block, lds, s, p, x, sx, y, d->n, d->k, R);
     else if (xp <= 2)
-      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 2>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 2, PREQ>), grid, block, lds, s, p, x, sx, y, d->n, d->k, R);
     else
-      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 6>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+      hipLaunchKernelGGL((gemv_a8_row_kernel<BITS, G, 6, PREQ>), grid, block, lds, s, p, x, sx, y, d->n, d->k, R);
   } else {
     return QX_E_UNSUPPORTED;
   }
@@ -295,7 +341,18 @@ int launch_gemv_a8_t(const qx_desc* d, const void* packed, const uint16_t* x, ui
 int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
   if (d->kind != QX_UNIFORM) return QX_E_UNSUPPORTED;
 #define QX_A8_CASE(B, G) \
-  if (d->bits == B && d->group == G) return launch_gemv_a8_t<B, G>(d, packed, x, y, s);
+  if (d->bits == B && d->group == G) return launch_gemv_a8_t<B, G, false>(d, packed, x, nullptr, y, s);
+  QX_A8_CASE(3, 32) QX_A8_CASE(3, 64) QX_A8_CASE(3, 128)
+  QX_A8_CASE(4, 32) QX_A8_CASE(4, 64) QX_A8_CASE(4, 128)
+#undef QX_A8_CASE
+  return QX_E_UNSUPPORTED;
+}
+
+int launch_gemv_a8q(const qx_desc* d, const void* packed, const int8_t* xq, const float* sx, uint16_t* y,
+                    hipStream_t s) {
+  if (d->kind != QX_UNIFORM) return QX_E_UNSUPPORTED;
+#define QX_A8_CASE(B, G) \
+  if (d->bits == B && d->group == G) return launch_gemv_a8_t<B, G, true>(d, packed, xq, sx, y, s);
   QX_A8_CASE(3, 32) QX_A8_CASE(3, 64) QX_A8_CASE(3, 128)
   QX_A8_CASE(4, 32) QX_A8_CASE(4, 64) QX_A8_CASE(4, 128)
 #undef QX_A8_CASE

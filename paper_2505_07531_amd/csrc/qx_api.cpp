@@ -228,6 +228,8 @@ int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq
   if (packed == nullptr || Xq == nullptr || sx == nullptr || Y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(Xq) || (reinterpret_cast<uintptr_t>(sx) & 3u) != 0 || !aligned2(Y))
     return QX_E_ARG;
+  if (m == 1 && d->k <= 88 * 128)  // one row: the A8 GEMV (v_dot4 on its staged int8 row)
+    return qx::launch_gemv_a8q(d, packed, Xq, sx, Y, stream);
   return qx::launch_gemm_a8(d, packed, m, Xq, sx, Y, stream);
 }
 

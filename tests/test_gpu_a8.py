@@ -10,7 +10,7 @@ import pytest
 import oracle
 from oracle import a8
 import qx_inputs as qi
-from helpers import TOL, activations, realistic_quant, to_dev
+from helpers import TOL, activations, random_quant, realistic_quant, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -155,3 +155,24 @@ def test_gemm_a8_rows_equal_gemv_a8_within_tolerance_and_repeat_bitwise(gpu):
     for r in range(6):
         y = pw.gemv_a8(Xd[r].contiguous()).cpu().numpy()
         assert oracle.normwise_rel_err(Y1[r], y.astype(np.float64)) <= TOL
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=lambda f: f"b{f[0]}g{f[1]}")
+@pytest.mark.parametrize("n,k", [(300, 4096), (70, 8192), (130, 11008), (37, 1152), (9, 1 << 14)])
+def test_gemm_a8_one_row_is_the_a8_gemv(gpu, fmt, n, k):
+    """m = 1 with k <= 88 chunks runs the A8 GEMV on the pre-quantized row: qx_gemv_a8's bits
+    (it quantizes the same fp16 row to the same codes); longer k runs the matrix cores and is
+    held to the oracle."""
+    qx = gpu
+    bits, g = fmt
+    q = random_quant(n, k, bits, g, 0, seed=n + k + g)
+    pw = qx.PackedWeight.from_quant(q)
+    x = activations(k, seed=k + bits)
+    xd = to_dev(x)
+    Xq, sx = qx.quantize_a8(xd[None, :].contiguous())
+    a = pw.gemm_a8(Xq, sx).cpu().numpy()[0]
+    if k <= 88 * 128:
+        b = pw.gemv_a8(xd).cpu().numpy()
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+    else:
+        assert oracle.normwise_rel_err(a, a8.gemv_a8(q.codes, g, q.scales, q.zeros, x)) <= TOL
