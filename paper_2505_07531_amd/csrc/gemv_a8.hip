@@ -288,6 +288,71 @@ __global__ __launch_bounds__(1024) void gemv_a8_row_kernel(const char* __restric
   }
 }
 
+// 2 <= m <= M pre-quantized rows (qx_gemm_a8 with a few rows): the segmented
+// small-batch structure of the fp16 kernel (R rows per block, k walked in
+// segments of S chunks, one item per lane and segment) with the int8 products of
+// the A8 GEMV, each chunk multiplied with the M staged rows. Vectors past m repeat
+// row m - 1 and are not stored. LDS: M staged segments (S chunks of 144 bytes
+// each), M*S*(128/G) group sums of xq, then R*S*M lane totals.
+template <int BITS, int G, int M>
+__global__ __launch_bounds__(512) void gemv_a8_multi_kernel(const char* __restrict__ packed,
+                                                            const int8_t* __restrict__ Xq,
+                                                            const float* __restrict__ sxp,
+                                                            uint16_t* __restrict__ Y, int n, int k, int m,
+                                                            int R, int S) {
+  extern __shared__ __align__(16) char smem[];
+  constexpr int NG = 128 / G;
+  const int C = k >> 7, G_row = k / G, nthreads = blockDim.x;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
+  const int row0 = blockIdx.x * R;
+  const int rows = min(R, n - row0);
+  const int xbytes = S * kX8Block;
+  float* gs = reinterpret_cast<float*>(smem + M * xbytes);  // [M][S*NG]
+  float* part = gs + M * S * NG;                             // [M][R*S]
+  const int t = threadIdx.x, r = t / S, c = t - r * S;
+  const int row = row0 + min(r, rows - 1);
+  const int nseg = (C + S - 1) / S;
+
+  float tot[M];
+#pragma unroll
+  for (int v = 0; v < M; ++v) tot[v] = 0.f;
+  for (int seg = 0; seg < nseg; ++seg) {
+    const int cs = min(S, C - seg * S);
+    // every thread holds at most one 8-byte piece per row and segment (the launcher
+    // makes blockDim.x >= 16*S)
+    u32x2 xr[M][1];
+#pragma unroll
+    for (int v = 0; v < M; ++v) {
+      const u32x2* src = reinterpret_cast<const u32x2*>(Xq + (size_t)min(v, m - 1) * k) + seg * S * 16;
+      xr[v][0] = src[min(t, cs * 16 - 1)];
+    }
+    CodesA8<BITS, G> it;
+    load_codes_a8<BITS, G>(it, packed, meta_off, row, seg * S + min(c, cs - 1), C, G_row);
+    if (seg > 0) __syncthreads();  // the previous segment is no longer read
+#pragma unroll
+    for (int v = 0; v < M; ++v) stage_xq_a8<BITS, G, 1>(xr[v], cs, smem + v * xbytes, gs + v * S * NG, nthreads);
+    __syncthreads();
+    if (c < cs) {
+#pragma unroll
+      for (int v = 0; v < M; ++v)
+        tot[v] += chunk_dot_a8<BITS, G>(it, smem + v * xbytes + c * kX8Block, gs + v * S * NG + c * NG);
+    }
+  }
+  if (r < rows) {
+#pragma unroll
+    for (int v = 0; v < M; ++v) part[v * R * S + t] = tot[v];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int mm = min(m, M), items = rows * mm;
+  for (int q = wave; q < items; q += nthreads >> 6) {
+    const int rr = q / mm, v = q - rr * mm;
+    float s = lane < S ? part[v * R * S + rr * S + lane] : 0.f;
+    s = wave_sum(s);
+    if (lane == 63) Y[(size_t)v * n + row0 + rr] = (uint16_t)float_to_half_bits(s * sxp[v]);
+  }
+}
+
 // Rows per block for the row kernel: the R (at most 8 for long rows) whose R*C items
 // leave the fewest idle lanes in blocks of at least 256 threads.
 void a8_row_shape(int C, int* R, int* threads) {
@@ -345,6 +410,40 @@ int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint
   QX_A8_CASE(3, 32) QX_A8_CASE(3, 64) QX_A8_CASE(3, 128)
   QX_A8_CASE(4, 32) QX_A8_CASE(4, 64) QX_A8_CASE(4, 128)
 #undef QX_A8_CASE
+  return QX_E_UNSUPPORTED;
+}
+
+int launch_gemv_a8_multi(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx,
+                         uint16_t* Y, hipStream_t s) {
+  if (d->kind != QX_UNIFORM || m < 2 || m > 4) return QX_E_UNSUPPORTED;
+  const int C = d->k / 128, S = std::min(C, 32);
+  // R rows per block: R*S lanes fill blocks of at least 512 threads best (16 rows at S = 32)
+  const int r_max = std::min(256, 512 / S);
+  int R = r_max;
+  double best_u = -1.0;
+  for (int r = 1; r <= r_max; ++r) {
+    const int th = 64 * ((r * S + 63) / 64);
+    if (th < 512 && r < r_max) continue;
+    const double u = (double)(r * S) / th;
+    if (u > best_u + 1e-9) { best_u = u; R = r; }
+  }
+  const int threads = 64 * ((R * S + 63) / 64);
+  if (threads < 16 * S || threads > 512) return QX_E_UNSUPPORTED;  // never with the shapes above
+  const int M = m <= 2 ? 2 : 4, NG = 128 / d->group;
+  const size_t lds = (size_t)M * S * kX8Block + (size_t)M * S * NG * 4 + (size_t)M * R * S * 4;
+  const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
+  const char* p = static_cast<const char*>(packed);
+#define QX_A8M_CASE(B, G)                                                                                  \
+  if (d->bits == B && d->group == G) {                                                                     \
+    if (M == 2)                                                                                            \
+      hipLaunchKernelGGL((gemv_a8_multi_kernel<B, G, 2>), grid, block, lds, s, p, Xq, sx, Y, d->n, d->k, m, R, S); \
+    else                                                                                                   \
+      hipLaunchKernelGGL((gemv_a8_multi_kernel<B, G, 4>), grid, block, lds, s, p, Xq, sx, Y, d->n, d->k, m, R, S); \
+    return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;                                            \
+  }
+  QX_A8M_CASE(3, 32) QX_A8M_CASE(3, 64) QX_A8M_CASE(3, 128)
+  QX_A8M_CASE(4, 32) QX_A8M_CASE(4, 64) QX_A8M_CASE(4, 128)
+#undef QX_A8M_CASE
   return QX_E_UNSUPPORTED;
 }
 

@@ -230,6 +230,10 @@ int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq
     return QX_E_ARG;
   if (m == 1 && d->k <= 88 * 128)  // one row: the A8 GEMV (v_dot4 on its staged int8 row)
     return qx::launch_gemv_a8q(d, packed, Xq, sx, Y, stream);
+  // a few rows: every code decoded once for all of them, where that measured faster
+  // than the matrix cores (m = 2 on any shape; m = 3, 4 when k > n)
+  if (m == 2 || (m >= 3 && m <= 4 && d->k > d->n))
+    return qx::launch_gemv_a8_multi(d, packed, m, Xq, sx, Y, stream);
   return qx::launch_gemm_a8(d, packed, m, Xq, sx, Y, stream);
 }
 

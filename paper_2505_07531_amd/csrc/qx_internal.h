@@ -40,6 +40,9 @@ int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint
 int launch_quantize_a8(int m, int k, const uint16_t* X, int8_t* Xq, float* sx, hipStream_t s);
 int launch_gemm_a8(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
                    hipStream_t s);
+// The small-batch A8 kernel for 2 <= m <= 4 pre-quantized rows (any k).
+int launch_gemv_a8_multi(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx,
+                         uint16_t* Y, hipStream_t s);
 // The A8 GEMV on one row already quantized (k <= 88*128).
 int launch_gemv_a8q(const qx_desc* d, const void* packed, const int8_t* xq, const float* sx, uint16_t* y,
                     hipStream_t s);

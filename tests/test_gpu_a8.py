@@ -176,3 +176,23 @@ def test_gemm_a8_one_row_is_the_a8_gemv(gpu, fmt, n, k):
         assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
     else:
         assert oracle.normwise_rel_err(a, a8.gemv_a8(q.codes, g, q.scales, q.zeros, x)) <= TOL
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=lambda f: f"b{f[0]}g{f[1]}")
+@pytest.mark.parametrize("m", [2, 3, 4])
+@pytest.mark.parametrize("n,k", [(4096, 4096), (300, 11008), (37, 1152), (9, 1 << 16)])
+def test_gemm_a8_small_batch(gpu, fmt, m, n, k):
+    """2 <= m <= 4 pre-quantized rows run the small-batch A8 kernel (each code decoded once
+    for all rows); every row against the oracle's A8 GEMV of that row."""
+    qx = gpu
+    bits, g = fmt
+    q = random_quant(n, k, bits, g, 0, seed=n + k + m)
+    X = _x_rows(m, k, seed=k + m)
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = qx.PackedWeight.from_quant(q).gemm_a8(Xq, sx).cpu().numpy()
+    for r in range(m):
+        ref = a8.gemv_a8(q.codes, g, q.scales, q.zeros, X[r])
+        if not np.any(ref):
+            assert not np.any(Y[r].astype(np.float32)), r
+            continue
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
