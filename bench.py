@@ -20,7 +20,7 @@ one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workl
 per-token activations), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
 rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
-matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
+matrix and the Q4X gate matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
 the same byte counts and empty grids: the floor of a one-launch GEMV) and
 --workload counters (the run that the FETCH_SIZE / WRITE_SIZE passes profile).
 """
@@ -561,7 +561,7 @@ def main():
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)
     elif args.workload == "a8":
-        for name in ("c1", "c2", "gateup"):
+        for name in ("c1", "c2", "gateup", "q4x.gate"):
             for a8 in (False, True):
                 print(json.dumps(bench_single_gemv(args, qx, name, a8)), flush=True)
     elif args.workload == "q4x":

@@ -10,6 +10,13 @@ symmetric scale for the whole vector.
   xq[k] = clamp(RNE(x[k] * inv), -127, 127)                int8, the product exact
   y[n]  = s_x * sum_j s[n,j] * sum_{k in group j} (q[n,k] - z[n,j]) * xq[k]
 
+Q4X with 8-bit activations (the paper's Table 2 runs Q4X with 8-bit RTN per-token
+activations): the same xq and s_x, and the fp16 entries of the selected
+sub-codebook in place of the integer levels,
+  y[n]  = s_x * sum_j s[n,j] * sum_{k in group j} CB[t[n,j]][q[n,k]] * xq[k]
+(the group scale multiplies the group's sum: the exact products s * CB, not W'
+rounded to binary16).
+
 The steps that decide an integer are the ones the GPU takes: the fp32 scale
 inv, and the nearest integer to the exact product of a binary16 x and the fp32
 inv (at most 35 significant bits, exact in fp64 here; one fused multiply-add
@@ -50,3 +57,20 @@ def gemv_a8(codes, group, scales, zeros, x16) -> np.ndarray:
     for g in range(G):
         per_group[:, g] = prod[:, g * group:(g + 1) * group].sum(axis=1)
     return float(s_x) * (s * per_group.astype(np.float64)).sum(axis=1)
+
+
+def gemv_a8_q4x(codes, scales, selectors, codebook, x16) -> np.ndarray:
+    """fp64 y [n] of a Q4X matrix (codes [n][k], binary16 scales [n][k/64], selectors
+    [n][k/64], binary16 codebook [4][16]) and fp16 x [k] quantized to 8 bits."""
+    codes = np.asarray(codes).astype(np.int64)
+    n, k = codes.shape
+    G = k // 64
+    xq, s_x = quantize_activation(x16)
+    s = np.asarray(scales, np.uint16).reshape(n, G).view(np.float16).astype(np.float64)
+    t = np.asarray(selectors).reshape(n, G).astype(np.int64)
+    cb = np.asarray(codebook, np.uint16).reshape(4, 16).view(np.float16).astype(np.float64)
+    j = np.arange(k) // 64
+    entries = cb[t[:, j], codes]                              # CB[t][q], exact binary16 values
+    prod = entries * xq.astype(np.float64)[None, :]
+    per_group = prod.reshape(n, G, 64).sum(axis=2)
+    return float(s_x) * (s * per_group).sum(axis=1)

@@ -1,0 +1,125 @@
+// Q4X GEMV with 8-bit activations: the paper's own runtime configuration (Q4X with
+// 8-bit round-to-nearest per-token activations, Table 2). The activation vector is
+// quantized as in the uniform A8 GEMV (amax = max |x|, xq = nearest integer to
+// x * fp32(127/amax), s_x = amax/127) and, since the Q4X levels are fp16 table
+// entries rather than integers, the integers xq are staged as exact binary16 values
+// and multiplied with the looked-up entries in fp32 like the fp16 Q4X GEMV:
+//   y[n] = s_x * sum_j s_j * sum_{k in group j} CB[t_j][q_k] * xq_k.
+// One (row, 128-code chunk) item per lane, R rows per block, partials through LDS
+// and one wave per row adding them in a fixed order (the row-kernel structure).
+#include "gemv_common.h"
+
+#include <algorithm>
+
+namespace qx {
+namespace {
+
+__device__ __forceinline__ float wave_max_q(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Nearest integer to x * inv (the product exact: one fused multiply-add with
+// 1.5 * 2^23, whose rounding step is 1), as an fp32 value.
+__device__ __forceinline__ float q8f(_Float16 v, float inv) {
+  return __builtin_fmaf((float)v, inv, 12582912.0f) - 12582912.0f;
+}
+
+template <int XP>
+__global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restrict__ packed,
+                                                           const uint16_t* __restrict__ x,
+                                                           uint16_t* __restrict__ y, int n, int k, int R) {
+  extern __shared__ __align__(16) char smem[];
+  __shared__ __align__(16) uint32_t q4lut[32];
+  __shared__ float red[16];
+  const int C = k >> 7, G_row = k / 64, nthreads = blockDim.x;
+  const size_t meta_off = (size_t)n * k / 2;
+  const int row0 = blockIdx.x * R;
+  const int rows = min(R, n - row0);
+  char* xs = smem;                                             // C * kXBlock bytes
+  float* part = reinterpret_cast<float*>(smem + C * kXBlock);  // R * C floats
+  const DecodeConsts kc = decode_consts();
+
+  u32x4 xr[XP];
+  load_x<XP>(x, 0, C, xr, nthreads);
+  const int t = threadIdx.x, r = t / C, c = t - r * C;
+  const bool valid = r < rows;
+  Item<4, QX_Q4X, 64> it;
+  load_item<4, QX_Q4X, 64>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+  stage_q4x_lut(packed, n, k, q4lut);
+
+  // amax over the vector (every block gets the same maximum: a maximum is exact)
+  h2_t mh = {(_Float16)0, (_Float16)0};
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {  // clamped duplicates of valid pieces leave the max unchanged
+    const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      mh = __builtin_elementwise_max(mh, __builtin_elementwise_abs(__builtin_bit_cast(h2_t, w[q])));
+  }
+  float m = wave_max_q(fmaxf((float)mh.x, (float)mh.y));
+  if ((t & 63) == 0) red[t >> 6] = m;
+  __syncthreads();
+  float amax = 0.f;
+  for (int i = 0; i < (nthreads >> 6); ++i) amax = fmaxf(amax, red[i]);
+  const float inv = amax > 0.f ? 127.f / amax : 0.f;
+  // the pieces as exact binary16 integers xq, staged in decoder order
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const h2_t h = __builtin_bit_cast(h2_t, w[q]);
+      const h2_t o = {(_Float16)q8f(h.x, inv), (_Float16)q8f(h.y, inv)};
+      w[q] = __builtin_bit_cast(uint32_t, o);
+    }
+    xr[i] = u32x4{w[0], w[1], w[2], w[3]};
+  }
+  store_x<4, QX_Q4X, 64, XP>(xr, C, xs, nullptr, nthreads);
+  __syncthreads();
+  if (valid) part[t] = chunk_dot<4, QX_Q4X, 64>(it, xs + c * kXBlock, nullptr, kc, q4lut);
+  __syncthreads();
+  const float sx = amax > 0.f ? amax / 127.f : 0.f;
+  const int wave = t >> 6, lane = t & 63;
+  for (int rr = wave; rr < rows; rr += nthreads >> 6) {
+    float v = 0.f;
+    for (int cc = lane; cc < C; cc += 64) v += part[rr * C + cc];
+    v = wave_sum(v);
+    if (lane == 63) y[row0 + rr] = (uint16_t)float_to_half_bits(v * sx);
+  }
+}
+
+}  // namespace
+
+// Q4X descriptors with k <= 88 chunks (as the uniform A8 GEMV).
+int launch_gemv_q4x_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  const int C = d->k / 128;
+  if (C > kMaxTileChunks) return QX_E_UNSUPPORTED;
+  // R rows per block: the R (at most 8 for long rows) whose R*C items leave the fewest
+  // idle lanes in blocks of at least 256 threads
+  const int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
+  int R = 1;
+  double best_u = -1.0;
+  for (int pass = 0; pass < 2 && best_u < 0; ++pass)
+    for (int r = 1; r <= r_max; ++r) {
+      const int th = 64 * ((r * C + 63) / 64);
+      if (pass == 0 && th < 256) continue;
+      const double u = (double)(r * C) / th;
+      if (u > best_u + 1e-9) { best_u = u; R = r; }
+    }
+  const int threads = 64 * ((R * C + 63) / 64);
+  const size_t lds = (size_t)C * kXBlock + (size_t)R * C * sizeof(float);
+  const int xp = (C * 16 + threads - 1) / threads;
+  const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
+  const char* p = static_cast<const char*>(packed);
+  if (xp <= 1)
+    hipLaunchKernelGGL((gemv_q4x_a8_kernel<1>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+  else if (xp <= 2)
+    hipLaunchKernelGGL((gemv_q4x_a8_kernel<2>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+  else  // blocks have >= 256 threads or C < 32, so xp <= ceil(88*16/256) = 6
+    hipLaunchKernelGGL((gemv_q4x_a8_kernel<6>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+  return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
+}
+
+}  // namespace qx

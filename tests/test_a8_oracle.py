@@ -70,3 +70,44 @@ def test_gemv_a8_close_to_a16():
     _, s_x = a8.quantize_activation(x)
     bound = float(s_x) / 2 * np.abs(w16).sum(axis=1) + 2.0**-11 * (np.abs(w16) @ np.abs(x.astype(np.float64)))
     assert np.all(np.abs(y8 - y16) <= bound * (1 + 1e-9))
+
+
+def test_gemv_a8_q4x_brute_force():
+    """Q4X with 8-bit activations: the loops of the definition, entry by entry."""
+    rng = np.random.default_rng(5)
+    n, k = 4, 192
+    G = k // 64
+    codes = rng.integers(0, 16, (n, k), dtype=np.uint8)
+    sel = rng.integers(0, 4, (n, G), dtype=np.uint8)
+    s = np.float16(rng.uniform(0.5, 2.0, (n, G))).view(np.uint16)
+    cb = np.float16(rng.standard_normal((4, 16))).view(np.uint16)
+    x = np.float16(rng.standard_normal(k))
+    y = a8.gemv_a8_q4x(codes, s, sel, cb, x)
+    xq, s_x = a8.quantize_activation(x)
+    cbf = cb.view(np.float16).astype(float)
+    sf = s.view(np.float16).astype(float)
+    for r in range(n):
+        tot = 0.0
+        for g in range(G):
+            acc = 0.0
+            for i in range(64 * g, 64 * g + 64):
+                acc += cbf[sel[r, g], codes[r, i]] * int(xq[i])
+            tot += sf[r, g] * acc
+        assert y[r] == pytest.approx(float(s_x) * tot, rel=1e-12, abs=1e-12)
+
+
+def test_gemv_a8_q4x_reduces_to_uniform_levels():
+    """A Q4X matrix whose sub-codebooks hold the integer levels q - z (z per selector) and
+    whose scales are the uniform scales gives the uniform A8 result."""
+    rng = np.random.default_rng(8)
+    n, k = 6, 256
+    G = k // 64
+    codes = rng.integers(0, 16, (n, k), dtype=np.uint8)
+    zsel = rng.integers(0, 4, (n, G), dtype=np.uint8)     # zero point 4 * selector
+    cb = np.stack([np.arange(16) - 4 * t for t in range(4)]).astype(np.float16).view(np.uint16)
+    s = np.float16(rng.uniform(0.01, 0.1, (n, G)))
+    x = np.float16(rng.standard_normal(k))
+    y = a8.gemv_a8_q4x(codes, s.view(np.uint16), zsel, cb, x)
+    z = (4 * zsel).astype(np.float16)
+    yu = a8.gemv_a8(codes, 64, s.view(np.uint16), z.view(np.uint16), x)
+    assert np.allclose(y, yu, rtol=1e-12, atol=1e-12)

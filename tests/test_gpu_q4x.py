@@ -158,3 +158,20 @@ def test_q4x_gemm_one_hot_rows_are_columns_of_w(gpu):
     assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))  # +0 sums of a -0 weight
     nz = ref.astype(np.float32) != 0
     assert np.array_equal(Y.view(np.uint16)[nz], ref.view(np.uint16)[nz])
+
+
+@pytest.mark.parametrize("shape", [(40, 1152), (130, 4096), (300, 11008), (4096, 4096), (37, 8192)],
+                         ids=lambda s: f"{s[0]}x{s[1]}")
+def test_q4x_gemv_a8_matches_oracle(gpu, shape):
+    """The paper's Q4X with 8-bit per-token activations (Table 2's configuration)."""
+    from oracle import a8
+    qx = gpu
+    n, k = shape
+    q = random_q4x(n, k, seed=n + k) if n * k > 10**7 else realistic_q4x(n, k, seed=n + k)
+    x = activations(k, seed=k + 1)
+    pw = _pack(qx, q)
+    y = pw.gemv_a8(to_dev(x)).cpu().numpy()
+    ref = a8.gemv_a8_q4x(q.codes, q.scales, q.selectors, q.codebook, x)
+    assert oracle.normwise_rel_err(y, ref) <= TOL
+    assert np.array_equal(y.view(np.uint16), pw.gemv_a8(to_dev(x)).cpu().numpy().view(np.uint16))
+    assert not np.any(pw.gemv_a8(to_dev(np.zeros(k, np.float16))).cpu().numpy())
