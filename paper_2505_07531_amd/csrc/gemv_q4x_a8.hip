@@ -5,8 +5,9 @@
 // entries rather than integers, the integers xq are staged as exact binary16 values
 // and multiplied with the looked-up entries in fp32 like the fp16 Q4X GEMV:
 //   y[n] = s_x * sum_j s_j * sum_{k in group j} CB[t_j][q_k] * xq_k.
-// One (row, 128-code chunk) item per lane, R rows per block, partials through LDS
-// and one wave per row adding them in a fixed order (the row-kernel structure).
+// One (row, 128-code chunk) item per lane; for k = 128*32 or 128*64 a row fills half
+// or all of a wave and is summed in registers (the wave-kernel structure), other k
+// up to 88 chunks use R rows per block with partials through LDS (the row kernel).
 #include "gemv_common.h"
 
 #include <algorithm>
@@ -24,6 +25,74 @@ __device__ __forceinline__ float wave_max_q(float v) {
 // 1.5 * 2^23, whose rounding step is 1), as an fp32 value.
 __device__ __forceinline__ float q8f(_Float16 v, float inv) {
   return __builtin_fmaf((float)v, inv, 12582912.0f) - 12582912.0f;
+}
+
+// Block-wide maximum magnitude of the staged x pieces (every thread gets it).
+template <int XP>
+__device__ __forceinline__ float block_amax(const u32x4 (&xr)[XP], float* red, int nthreads) {
+  h2_t mh = {(_Float16)0, (_Float16)0};
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {  // clamped duplicates of valid pieces leave the max unchanged
+    const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      mh = __builtin_elementwise_max(mh, __builtin_elementwise_abs(__builtin_bit_cast(h2_t, w[q])));
+  }
+  const float m = wave_max_q(fmaxf((float)mh.x, (float)mh.y));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  float amax = 0.f;
+  for (int i = 0; i < (nthreads >> 6); ++i) amax = fmaxf(amax, red[i]);
+  return amax;
+}
+
+// The pieces as exact binary16 integers xq = nearest integer to x * inv.
+template <int XP>
+__device__ __forceinline__ void quantize_pieces(u32x4 (&xr)[XP], float inv) {
+#pragma unroll
+  for (int i = 0; i < XP; ++i) {
+    uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const h2_t h = __builtin_bit_cast(h2_t, w[q]);
+      const h2_t o = {(_Float16)q8f(h.x, inv), (_Float16)q8f(h.y, inv)};
+      w[q] = __builtin_bit_cast(uint32_t, o);
+    }
+    xr[i] = u32x4{w[0], w[1], w[2], w[3]};
+  }
+}
+
+// k = 128*LPR with LPR in {32, 64}: as the fp16 wave kernel, a row's chunks fill LPR
+// lanes of one wave and are summed with DPP; the block's WPB waves stage x once.
+template <int LPR, int WPB>
+__global__ __launch_bounds__(64 * WPB) void gemv_q4x_a8_wave_kernel(const char* __restrict__ packed,
+                                                                    const uint16_t* __restrict__ x,
+                                                                    uint16_t* __restrict__ y, int n) {
+  constexpr int C = LPR, NT = 64 * WPB, RPW = 64 / LPR, RPB = WPB * RPW;
+  constexpr int XP = (C * 16 + NT - 1) / NT;
+  __shared__ __align__(16) char xs[C * kXBlock];
+  __shared__ __align__(16) uint32_t q4lut[32];
+  __shared__ float red[WPB];
+  const int k = C * 128;
+  const size_t meta_off = (size_t)n * k / 2;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & (LPR - 1);
+  const int row = blockIdx.x * RPB + wave * RPW + lane / LPR;
+  const DecodeConsts kc = decode_consts();
+
+  u32x4 xr[XP];
+  load_x<XP>(x, 0, C, xr, NT);
+  Item<4, QX_Q4X, 64> it;
+  load_item<4, QX_Q4X, 64>(it, packed, meta_off, min(row, n - 1), c, C, k / 64);
+  stage_q4x_lut(packed, n, k, q4lut);
+  const float amax = block_amax<XP>(xr, red, NT);
+  quantize_pieces<XP>(xr, amax > 0.f ? 127.f / amax : 0.f);
+  store_x<4, QX_Q4X, 64, XP, C * 16 % NT == 0>(xr, C, xs, nullptr, NT);
+  __syncthreads();
+  float v = chunk_dot<4, QX_Q4X, 64>(it, xs + c * kXBlock, nullptr, kc, q4lut);
+  v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
+  const float sx = amax > 0.f ? amax / 127.f : 0.f;
+  if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v * sx);
 }
 
 template <int XP>
@@ -49,33 +118,10 @@ __global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restric
   load_item<4, QX_Q4X, 64>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
   stage_q4x_lut(packed, n, k, q4lut);
 
-  // amax over the vector (every block gets the same maximum: a maximum is exact)
-  h2_t mh = {(_Float16)0, (_Float16)0};
-#pragma unroll
-  for (int i = 0; i < XP; ++i) {  // clamped duplicates of valid pieces leave the max unchanged
-    const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      mh = __builtin_elementwise_max(mh, __builtin_elementwise_abs(__builtin_bit_cast(h2_t, w[q])));
-  }
-  float m = wave_max_q(fmaxf((float)mh.x, (float)mh.y));
-  if ((t & 63) == 0) red[t >> 6] = m;
-  __syncthreads();
-  float amax = 0.f;
-  for (int i = 0; i < (nthreads >> 6); ++i) amax = fmaxf(amax, red[i]);
-  const float inv = amax > 0.f ? 127.f / amax : 0.f;
+  // amax over the vector (every block gets the same maximum: a maximum is exact), then
   // the pieces as exact binary16 integers xq, staged in decoder order
-#pragma unroll
-  for (int i = 0; i < XP; ++i) {
-    uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const h2_t h = __builtin_bit_cast(h2_t, w[q]);
-      const h2_t o = {(_Float16)q8f(h.x, inv), (_Float16)q8f(h.y, inv)};
-      w[q] = __builtin_bit_cast(uint32_t, o);
-    }
-    xr[i] = u32x4{w[0], w[1], w[2], w[3]};
-  }
+  const float amax = block_amax<XP>(xr, red, nthreads);
+  quantize_pieces<XP>(xr, amax > 0.f ? 127.f / amax : 0.f);
   store_x<4, QX_Q4X, 64, XP>(xr, C, xs, nullptr, nthreads);
   __syncthreads();
   if (valid) part[t] = chunk_dot<4, QX_Q4X, 64>(it, xs + c * kXBlock, nullptr, kc, q4lut);
@@ -96,6 +142,17 @@ __global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restric
 int launch_gemv_q4x_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
   const int C = d->k / 128;
   if (C > kMaxTileChunks) return QX_E_UNSUPPORTED;
+  if (C == 32 || C == 64) {
+    constexpr int WPB = 4;
+    const int rpb = WPB * 64 / C;
+    const dim3 grid((unsigned)((d->n + rpb - 1) / rpb)), block(64 * WPB);
+    const char* p = static_cast<const char*>(packed);
+    if (C == 32)
+      hipLaunchKernelGGL((gemv_q4x_a8_wave_kernel<32, WPB>), grid, block, 0, s, p, x, y, d->n);
+    else
+      hipLaunchKernelGGL((gemv_q4x_a8_wave_kernel<64, WPB>), grid, block, 0, s, p, x, y, d->n);
+    return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
+  }
   // R rows per block: the R (at most 8 for long rows) whose R*C items leave the fewest
   // idle lanes in blocks of at least 256 threads
   const int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
