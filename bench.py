@@ -20,7 +20,9 @@ one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workl
 per-token activations), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
 rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
-matrix and the Q4X gate matrix with fp16 and with int8 activations, one line each), --workload floor (plain read of
+matrix and the Q4X gate matrix with fp16 and with int8 activations, one line each), --workload tp8
+(one GPU's share of the decode step at 8-way tensor parallelism, and c2 split 8 ways by
+rows; the collectives are not run), --workload floor (plain read of
 the same byte counts and empty grids: the floor of a one-launch GEMV) and
 --workload counters (the run that the FETCH_SIZE / WRITE_SIZE passes profile).
 """
@@ -341,6 +343,73 @@ def bench_decode_batch(args, qx):
     return lines
 
 
+def bench_tp8_share(args, qx):
+    """One GPU's share of the decode step under 8-way tensor parallelism, at its real
+    shapes: q|k|v and gate|up split by rows (512 rows of each of q, k, v, 1376 of gate and
+    of up), o and down split along k (512, and 11008 / 8 padded to 11 chunks = 1408; these
+    are synthetic matrices of the shard shape drawn like o and down), 128 launches per step
+    replayed from a HIP graph; and the c2 matrix split 8 ways by rows (1376x4096). The
+    all-reduces after o and down, and everything between GPUs, are not run."""
+    import torch
+    from qx_inputs import configs
+    dev = torch.device("cuda:0")
+    P, H, F = 8, configs.HIDDEN, configs.MLP
+    kd = -(-F // P // 128) * 128
+    launches, packed = [], 0
+    for l in range(configs.LAYERS):
+        qkv = concat_rows([configs.c4_matrix(l, m).quantized(0, H // P) for m in ("q", "k", "v")])
+        gu = concat_rows([configs.c4_matrix(l, m).quantized(0, F // P) for m in ("gate", "up")])
+        o = configs.MatrixSpec(f"L{l}.o/{P}", H, H // P, "laplace", configs.LAPLACE_B, 5, 2 * l, 3, 128,
+                               configs.CODEBOOK).quantized()
+        dn = configs.MatrixSpec(f"L{l}.down/{P}", H, kd, "t4", configs.T4_STD, 5, 2 * l + 1, 4, 128,
+                                configs.UNIFORM).quantized()
+        xs = [configs.c4_activation(l, 0), configs.c4_activation(l, 1)[:H // P], configs.c4_activation(l, 2),
+              configs.c4_activation(l, 3)[:kd]]
+        for q, x in zip((qkv, o, gu, dn), xs):
+            pw = qx.PackedWeight.from_quant(q, device=dev)
+            packed += pw.data.numel()
+            launches.append((pw, torch.from_numpy(np.ascontiguousarray(x)).to(dev),
+                             torch.empty(q.n, dtype=torch.float16, device=dev)))
+    def launch():
+        for pw, x, y in launches:
+            qx.qx_gemv(pw.desc, pw.data, x, y)
+    stream = torch.cuda.Stream()
+    ms = time_graph(launch, stream, args.steps, args.warmup)
+    log(f"tp8 share: {ms * 1e3:.1f} us per step, {packed} packed bytes")
+    lines = [{"metric": "one GPU's share of the 7B decode step at 8-way tensor parallelism (us per step)",
+              "value": round(ms * 1e3, 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
+              "warmup": args.warmup, "ms_per_step": round(ms, 6), "higher_is_better": False,
+              "scaling": "strong", "vs_baseline": None, "dtype": "f16",
+              "data": "synthetic (seeded Philox weights and activations)",
+              "config": {"workload": "7B decoder decode step, batch 1, the share of one of 8 GPUs: per layer "
+                                     "q|k|v 1536x4096 and o 4096x512 codebook-3 g128, gate|up 2752x4096 and "
+                                     "down 4096x1408 uniform-4 g128 (128 launches, HIP graph replay); "
+                                     "collectives not run", "packed_bytes_per_step": packed},
+              "effective_weight_GBps": round(packed / (ms * 1e-3) / 1e9, 1)}]
+    spec, x = configs.c2()
+    q = spec.quantized(0, F // P)
+    d = qx.desc(q.n, q.k, q.bits, q.group, q.kind)
+    blob = qx.qx_pack_layout(d, q.codes, q.scales, q.zeros, q.codebook)
+    base = torch.from_numpy(blob).to(dev)
+    copies = [base] + [base.clone() for _ in range(max(2, -(-(512 << 20) // blob.size)) - 1)]
+    xd = torch.from_numpy(x).to(dev)
+    y = torch.empty(q.n, dtype=torch.float16, device=dev)
+    def launch_c2():
+        for c in copies:
+            qx.qx_gemv(d, c, xd, y)
+    ms2 = time_graph(launch_c2, stream, max(3, args.steps // len(copies)), 2) / len(copies)
+    gbs = (blob.size + 2 * (q.n + q.k)) / (ms2 * 1e-3) / 1e9
+    lines.append({"metric": "batch-1 qGEMV effective HBM GB/s (c2, one of 8 row shards)", "value": round(gbs, 2),
+                  "unit": "GB/s", "n_gpus": 1, "steps": len(copies) * max(3, args.steps // len(copies)),
+                  "warmup": 2 * len(copies), "ms_per_step": round(ms2, 6), "higher_is_better": True,
+                  "scaling": "strong", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+                  "config": {"workload": f"c2 rows 0-{q.n - 1}: {q.n}x{q.k} 3-bit uniform g64, graph of "
+                                         f"back-to-back launches over {len(copies)} copies",
+                             "packed_bytes": int(blob.size)},
+                  "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "avg_launch_us": round(ms2 * 1e3, 3)})
+    return lines
+
+
 def rotated_copies(qx, spec, device, min_total=512 << 20):
     q = spec.quantized()
     d = qx.desc(q.n, q.k, q.bits, q.group, q.kind)
@@ -520,7 +589,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
                     choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "c5a8", "q4x", "a8",
-                             "counters", "floor"])
+                             "tp8", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -551,6 +620,9 @@ def main():
         print(json.dumps(bench_kernel_counters(args, qx)), flush=True)
     elif args.workload == "floor":
         print(json.dumps(bench_floor(args, qx)), flush=True)
+    elif args.workload == "tp8":
+        for line in bench_tp8_share(args, qx):
+            print(json.dumps(line), flush=True)
     elif args.workload == "batch":
         for line in bench_decode_batch(args, qx):
             print(json.dumps(line), flush=True)

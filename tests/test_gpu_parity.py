@@ -70,7 +70,8 @@ def test_dequant_configs_bit_exact(gpu, make):
 
 # covers every GEMV kernel path: rows of 32 or 64 chunks (in-wave reduction), rows of
 # up to 88 chunks (one chunk per lane), longer rows (K tiles), ragged row counts
-GEMV_SHAPES = SHAPES + [(33, 12288), (9, 16384), (260, 1024), (19, 8192), (1001, 11008)]
+GEMV_SHAPES = SHAPES + [(33, 12288), (9, 16384), (260, 1024), (19, 8192), (1001, 11008),
+                        (300, 512), (70, 1408)]  # 8-way shards of o (k 512) and down (k 11 chunks)
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
