@@ -17,6 +17,12 @@ sub-codebook in place of the integer levels,
 (the group scale multiplies the group's sum: the exact products s * CB, not W'
 rounded to binary16).
 
+Per-group codebooks with 8-bit activations (QuantX picks uniform or non-uniform
+groups per layer, Section 2.2, and runs its W3A8 configurations, Table 1, with
+either): the same xq and s_x, and the group's fp16 table entries, which are W'
+exactly,
+  y[n]  = s_x * sum_k C[n, j(k)][q[n,k]] * xq[k]          (j(k) = k // g).
+
 The steps that decide an integer are the ones the GPU takes: the fp32 scale
 inv, and the nearest integer to the exact product of a binary16 x and the fp32
 inv (at most 35 significant bits, exact in fp64 here; one fused multiply-add
@@ -74,3 +80,17 @@ def gemv_a8_q4x(codes, scales, selectors, codebook, x16) -> np.ndarray:
     prod = entries * xq.astype(np.float64)[None, :]
     per_group = prod.reshape(n, G, 64).sum(axis=2)
     return float(s_x) * (s * per_group).sum(axis=1)
+
+
+def gemv_a8_codebook(codes, group, codebook, x16) -> np.ndarray:
+    """fp64 y [n] of per-group codebook codes [n][k] (binary16 tables [n][k/g][2^b])
+    and fp16 x [k] quantized to 8 bits."""
+    codes = np.asarray(codes).astype(np.int64)
+    n, k = codes.shape
+    G = k // group
+    xq, s_x = quantize_activation(x16)
+    E = np.asarray(codebook).shape[-1]
+    cb = np.asarray(codebook, np.uint16).reshape(n, G, E).view(np.float16).astype(np.float64)
+    j = np.arange(k) // group
+    entries = cb[np.arange(n)[:, None], j[None, :], codes]   # C[n, j(k)][q], exact binary16 values
+    return float(s_x) * (entries * xq.astype(np.float64)[None, :]).sum(axis=1)

@@ -111,3 +111,52 @@ def test_gemv_a8_q4x_reduces_to_uniform_levels():
     z = (4 * zsel).astype(np.float16)
     yu = a8.gemv_a8(codes, 64, s.view(np.uint16), z.view(np.uint16), x)
     assert np.allclose(y, yu, rtol=1e-12, atol=1e-12)
+
+
+# ---- per-group codebooks with 8-bit activations
+
+@pytest.mark.parametrize("bits,group", [(3, 128), (3, 32), (4, 64)])
+def test_gemv_a8_codebook_brute_force(bits, group):
+    rng = np.random.default_rng(bits + group)
+    n, k = 4, 256
+    q = qi.quantize_codebook(qi.weights("laplace", 0.008, 5, bits, n, k), bits, group)
+    x = np.float16(rng.standard_normal(k))
+    y = a8.gemv_a8_codebook(q.codes, group, q.codebook, x)
+    xq, s_x = a8.quantize_activation(x)
+    cb = q.codebook.reshape(n, k // group, 1 << bits).view(np.float16)
+    for r in range(n):
+        tot = 0.0
+        for i in range(k):
+            tot += float(cb[r, i // group, q.codes[r, i]]) * int(xq[i])
+        assert y[r] == pytest.approx(float(s_x) * tot, rel=1e-12, abs=1e-15)
+
+
+def test_gemv_a8_codebook_reduces_to_uniform():
+    """Tables holding the uniform levels s (q - z) (exact in binary16 for a power-of-two s)
+    give the integer-domain uniform result exactly."""
+    rng = np.random.default_rng(3)
+    n, k, bits, group = 6, 512, 3, 64
+    G = k // group
+    codes = rng.integers(0, 8, (n, k)).astype(np.uint8)
+    z = rng.integers(0, 8, (n, G))
+    s = 2.0 ** rng.integers(-12, -4, (n, G))
+    levels = s[:, :, None] * (np.arange(8)[None, None, :] - z[:, :, None])
+    cb = levels.astype(np.float16).view(np.uint16)
+    assert np.array_equal(cb.view(np.float16).astype(np.float64), levels)  # the levels are exact
+    x = np.float16(rng.standard_normal(k))
+    y_cb = a8.gemv_a8_codebook(codes, group, cb, x)
+    y_u = a8.gemv_a8(codes, group, s.astype(np.float16).view(np.uint16), z.astype(np.float16).view(np.uint16), x)
+    assert np.allclose(y_cb, y_u, rtol=1e-14, atol=0)
+
+
+def test_gemv_a8_codebook_error_bound():
+    """Against the fp16-activation product of the same W': |y_a8 - W' x| <= sum |W'| s_x / 2 per
+    row (each xq is within half a step of x / s_x), up to the rounding of s_x."""
+    n, k, bits, group = 20, 1024, 3, 128
+    q = qi.quantize_codebook(qi.weights("laplace", 0.008, 6, 1, n, k), bits, group)
+    x = qi.activations(6, 2, k, outliers=np.arange(0, k, 101))
+    w = oracle.dequant(q.codes, group, 1, codebook=q.codebook).astype(np.float64)
+    y = a8.gemv_a8_codebook(q.codes, group, q.codebook, x)
+    _, s_x = a8.quantize_activation(x)
+    bound = np.abs(w).sum(axis=1) * float(s_x) * (0.5 + 1e-5)
+    assert np.all(np.abs(y - w @ x.astype(np.float64)) <= bound)
