@@ -19,7 +19,7 @@ configs, rotated over enough copies to defeat the 256 MB last-level cache),
 one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workload c5a8 (the same with int8
 per-token activations), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
-rotated over copies like c1-c3), --workload a8 (c1, c2 and the 22016x4096 gate|up
+rotated over copies like c1-c3), --workload a8 (c1, c2, c3, the 22016x4096 gate|up
 matrix and the Q4X gate matrix with fp16 and with int8 activations, one line each), --workload tp8
 (one GPU's share of the decode step at 8-way tensor parallelism, and c2 split 8 ways by
 rows; the collectives are not run), --workload floor (plain read of
@@ -633,7 +633,7 @@ def main():
         for line in bench_gemm(args, qx):
             print(json.dumps(line), flush=True)
     elif args.workload == "a8":
-        for name in ("c1", "c2", "gateup", "q4x.gate"):
+        for name in ("c1", "c2", "c3", "gateup", "q4x.gate"):
             for a8 in (False, True):
                 print(json.dumps(bench_single_gemv(args, qx, name, a8)), flush=True)
     elif args.workload == "q4x":

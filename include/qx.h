@@ -159,7 +159,7 @@ int qx_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y
             hipStream_t stream);
 
 /*
- * qx_gemv_a8 -- y = W' x with x quantized to 8 bits (device; uniform and Q4X kinds).
+ * qx_gemv_a8 -- y = W' x with x quantized to 8 bits (device; every kind).
  * Passage: activations are quantized to 8 bits and not below (Section 2.4);
  * the W3A8 configurations of Table 1 and Table 2's runs use 8-bit
  * round-to-nearest per-token activations.
@@ -168,10 +168,13 @@ int qx_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y
  *     scale s_x = amax/127; amax = 0 gives y = 0);
  *   y fp16 [n] = s_x * sum_j s_j * sum_{k in group j} (q - z_j) * xq, the
  *     integer sums exact, scaled in fp32 and rounded to nearest-even;
+ *   codebook (QuantX's non-uniform groups, Section 2.2, in its W3A8
+ *     configurations): y = s_x * sum_k C_j[q] * xq, fp32 products of the fp16
+ *     table entries and the integers xq, sums in fp32;
  *   Q4X (the paper's Q4X with 8-bit activations, Table 2): y = s_x * sum_j s_j *
  *     sum_{k in group j} CB[t_j][q] * xq, fp32 products of the fp16 entries and
  *     the integers xq, sums in fp32.
- * Uniform and Q4X descriptors with k <= 88*128 only (QX_E_UNSUPPORTED otherwise).
+ * Descriptors with k <= 88*128 only (QX_E_UNSUPPORTED otherwise).
  * Deterministic; n = 0 is a no-op; buffers and alignment as for qx_gemv.
  */
 int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,

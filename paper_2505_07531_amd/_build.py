@@ -14,7 +14,7 @@ LIB = os.path.join(PKG, "libqx.so")
 PROBE_LIB = os.path.join(PKG, "libqxprobe.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["qx_api.cpp", "dequant.hip", "gemv.hip", "gemv_a8.hip", "gemv_q4x_a8.hip", "gemv_multi.hip",
+SOURCES = ["qx_api.cpp", "dequant.hip", "gemv.hip", "gemv_a8.hip", "gemv_lut_a8.hip", "gemv_multi.hip",
            "gemm.hip", "gemm_a8.hip"]
 PROBE_SOURCES = ["bw_probe.hip"]
 ARCH = "gfx950"

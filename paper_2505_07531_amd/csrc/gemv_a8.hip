@@ -404,8 +404,7 @@ int launch_gemv_a8_t(const qx_desc* d, const void* packed, const void* x, const 
 }  // namespace
 
 int launch_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
-  if (d->kind == QX_Q4X) return launch_gemv_q4x_a8(d, packed, x, y, s);
-  if (d->kind != QX_UNIFORM) return QX_E_UNSUPPORTED;
+  if (d->kind != QX_UNIFORM) return launch_gemv_lut_a8(d, packed, x, y, s);
 #define QX_A8_CASE(B, G) \
   if (d->bits == B && d->group == G) return launch_gemv_a8_t<B, G, false>(d, packed, x, nullptr, y, s);
   QX_A8_CASE(3, 32) QX_A8_CASE(3, 64) QX_A8_CASE(3, 128)

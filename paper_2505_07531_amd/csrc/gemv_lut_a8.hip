@@ -1,10 +1,13 @@
-// Q4X GEMV with 8-bit activations: the paper's own runtime configuration (Q4X with
-// 8-bit round-to-nearest per-token activations, Table 2). The activation vector is
-// quantized as in the uniform A8 GEMV (amax = max |x|, xq = nearest integer to
-// x * fp32(127/amax), s_x = amax/127) and, since the Q4X levels are fp16 table
-// entries rather than integers, the integers xq are staged as exact binary16 values
-// and multiplied with the looked-up entries in fp32 like the fp16 Q4X GEMV:
-//   y[n] = s_x * sum_j s_j * sum_{k in group j} CB[t_j][q_k] * xq_k.
+// GEMV with 8-bit activations for the table formats: per-group codebooks (QuantX's
+// non-uniform groups, Section 2.2, in its W3A8 configurations, Table 1) and Q4X
+// (the paper's own runtime configuration: Q4X with 8-bit round-to-nearest per-token
+// activations, Table 2). The activation vector is quantized as in the uniform A8
+// GEMV (amax = max |x|, xq = nearest integer to x * fp32(127/amax), s_x = amax/127)
+// and, since table levels are fp16 entries rather than integers, the integers xq
+// are staged as exact binary16 values and multiplied with the looked-up entries in
+// fp32 like the fp16 GEMV of the same format:
+//   codebook  y[n] = s_x * sum_k C[n, j(k)][q_k] * xq_k
+//   Q4X       y[n] = s_x * sum_j s_j * sum_{k in group j} CB[t_j][q_k] * xq_k.
 // One (row, 128-code chunk) item per lane; for k = 128*32 or 128*64 a row fills half
 // or all of a wave and is summed in registers (the wave-kernel structure), other k
 // up to 88 chunks use R rows per block with partials through LDS (the row kernel).
@@ -64,17 +67,17 @@ __device__ __forceinline__ void quantize_pieces(u32x4 (&xr)[XP], float inv) {
 
 // k = 128*LPR with LPR in {32, 64}: as the fp16 wave kernel, a row's chunks fill LPR
 // lanes of one wave and are summed with DPP; the block's WPB waves stage x once.
-template <int LPR, int WPB>
-__global__ __launch_bounds__(64 * WPB) void gemv_q4x_a8_wave_kernel(const char* __restrict__ packed,
+template <int BITS, int KIND, int G, int LPR, int WPB>
+__global__ __launch_bounds__(64 * WPB) void gemv_lut_a8_wave_kernel(const char* __restrict__ packed,
                                                                     const uint16_t* __restrict__ x,
                                                                     uint16_t* __restrict__ y, int n) {
   constexpr int C = LPR, NT = 64 * WPB, RPW = 64 / LPR, RPB = WPB * RPW;
   constexpr int XP = (C * 16 + NT - 1) / NT;
   __shared__ __align__(16) char xs[C * kXBlock];
-  __shared__ __align__(16) uint32_t q4lut[32];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   __shared__ float red[WPB];
   const int k = C * 128;
-  const size_t meta_off = (size_t)n * k / 2;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c = lane & (LPR - 1);
   const int row = blockIdx.x * RPB + wave * RPW + lane / LPR;
@@ -82,28 +85,28 @@ __global__ __launch_bounds__(64 * WPB) void gemv_q4x_a8_wave_kernel(const char* 
 
   u32x4 xr[XP];
   load_x<XP>(x, 0, C, xr, NT);
-  Item<4, QX_Q4X, 64> it;
-  load_item<4, QX_Q4X, 64>(it, packed, meta_off, min(row, n - 1), c, C, k / 64);
-  stage_q4x_lut(packed, n, k, q4lut);
+  Item<BITS, KIND, G> it;
+  load_item<BITS, KIND, G>(it, packed, meta_off, min(row, n - 1), c, C, k / G);
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);
   const float amax = block_amax<XP>(xr, red, NT);
   quantize_pieces<XP>(xr, amax > 0.f ? 127.f / amax : 0.f);
-  store_x<4, QX_Q4X, 64, XP, C * 16 % NT == 0>(xr, C, xs, nullptr, NT);
+  store_x<BITS, KIND, G, XP, C * 16 % NT == 0>(xr, C, xs, nullptr, NT);
   __syncthreads();
-  float v = chunk_dot<4, QX_Q4X, 64>(it, xs + c * kXBlock, nullptr, kc, q4lut);
+  float v = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, nullptr, kc, q4lut);
   v = (LPR == 32) ? half_wave_sum(v) : wave_sum(v);
   const float sx = amax > 0.f ? amax / 127.f : 0.f;
   if ((lane & (LPR - 1)) == LPR - 1 && row < n) y[row] = (uint16_t)float_to_half_bits(v * sx);
 }
 
-template <int XP>
-__global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restrict__ packed,
-                                                           const uint16_t* __restrict__ x,
-                                                           uint16_t* __restrict__ y, int n, int k, int R) {
+template <int BITS, int KIND, int G, int XP>
+__global__ __launch_bounds__(1024) void gemv_lut_a8_row_kernel(const char* __restrict__ packed,
+                                                               const uint16_t* __restrict__ x,
+                                                               uint16_t* __restrict__ y, int n, int k, int R) {
   extern __shared__ __align__(16) char smem[];
-  __shared__ __align__(16) uint32_t q4lut[32];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   __shared__ float red[16];
-  const int C = k >> 7, G_row = k / 64, nthreads = blockDim.x;
-  const size_t meta_off = (size_t)n * k / 2;
+  const int C = k >> 7, G_row = k / G, nthreads = blockDim.x;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
   const int row0 = blockIdx.x * R;
   const int rows = min(R, n - row0);
   char* xs = smem;                                             // C * kXBlock bytes
@@ -114,17 +117,17 @@ __global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restric
   load_x<XP>(x, 0, C, xr, nthreads);
   const int t = threadIdx.x, r = t / C, c = t - r * C;
   const bool valid = r < rows;
-  Item<4, QX_Q4X, 64> it;
-  load_item<4, QX_Q4X, 64>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
-  stage_q4x_lut(packed, n, k, q4lut);
+  Item<BITS, KIND, G> it;
+  load_item<BITS, KIND, G>(it, packed, meta_off, row0 + min(r, rows - 1), c, C, G_row);
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);
 
   // amax over the vector (every block gets the same maximum: a maximum is exact), then
   // the pieces as exact binary16 integers xq, staged in decoder order
   const float amax = block_amax<XP>(xr, red, nthreads);
   quantize_pieces<XP>(xr, amax > 0.f ? 127.f / amax : 0.f);
-  store_x<4, QX_Q4X, 64, XP>(xr, C, xs, nullptr, nthreads);
+  store_x<BITS, KIND, G, XP>(xr, C, xs, nullptr, nthreads);
   __syncthreads();
-  if (valid) part[t] = chunk_dot<4, QX_Q4X, 64>(it, xs + c * kXBlock, nullptr, kc, q4lut);
+  if (valid) part[t] = chunk_dot<BITS, KIND, G>(it, xs + c * kXBlock, nullptr, kc, q4lut);
   __syncthreads();
   const float sx = amax > 0.f ? amax / 127.f : 0.f;
   const int wave = t >> 6, lane = t & 63;
@@ -136,21 +139,19 @@ __global__ __launch_bounds__(1024) void gemv_q4x_a8_kernel(const char* __restric
   }
 }
 
-}  // namespace
-
-// Q4X descriptors with k <= 88 chunks (as the uniform A8 GEMV).
-int launch_gemv_q4x_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
+template <int BITS, int KIND, int G>
+static int launch_lut_a8_t(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
   const int C = d->k / 128;
   if (C > kMaxTileChunks) return QX_E_UNSUPPORTED;
+  const char* p = static_cast<const char*>(packed);
   if (C == 32 || C == 64) {
     constexpr int WPB = 4;
     const int rpb = WPB * 64 / C;
     const dim3 grid((unsigned)((d->n + rpb - 1) / rpb)), block(64 * WPB);
-    const char* p = static_cast<const char*>(packed);
     if (C == 32)
-      hipLaunchKernelGGL((gemv_q4x_a8_wave_kernel<32, WPB>), grid, block, 0, s, p, x, y, d->n);
+      hipLaunchKernelGGL((gemv_lut_a8_wave_kernel<BITS, KIND, G, 32, WPB>), grid, block, 0, s, p, x, y, d->n);
     else
-      hipLaunchKernelGGL((gemv_q4x_a8_wave_kernel<64, WPB>), grid, block, 0, s, p, x, y, d->n);
+      hipLaunchKernelGGL((gemv_lut_a8_wave_kernel<BITS, KIND, G, 64, WPB>), grid, block, 0, s, p, x, y, d->n);
     return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
   }
   // R rows per block: the R (at most 8 for long rows) whose R*C items leave the fewest
@@ -169,14 +170,27 @@ int launch_gemv_q4x_a8(const qx_desc* d, const void* packed, const uint16_t* x, 
   const size_t lds = (size_t)C * kXBlock + (size_t)R * C * sizeof(float);
   const int xp = (C * 16 + threads - 1) / threads;
   const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
-  const char* p = static_cast<const char*>(packed);
   if (xp <= 1)
-    hipLaunchKernelGGL((gemv_q4x_a8_kernel<1>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+    hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 1>), grid, block, lds, s, p, x, y, d->n, d->k, R);
   else if (xp <= 2)
-    hipLaunchKernelGGL((gemv_q4x_a8_kernel<2>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+    hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 2>), grid, block, lds, s, p, x, y, d->n, d->k, R);
   else  // blocks have >= 256 threads or C < 32, so xp <= ceil(88*16/256) = 6
-    hipLaunchKernelGGL((gemv_q4x_a8_kernel<6>), grid, block, lds, s, p, x, y, d->n, d->k, R);
+    hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 6>), grid, block, lds, s, p, x, y, d->n, d->k, R);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
+}
+
+}  // namespace
+
+// Codebook and Q4X descriptors with k <= 88 chunks (as the uniform A8 GEMV).
+int launch_gemv_lut_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  if (d->kind == QX_Q4X) return launch_lut_a8_t<4, QX_Q4X, 64>(d, packed, x, y, s);
+  if (d->kind != QX_CODEBOOK) return QX_E_UNSUPPORTED;
+#define QX_LUT_A8_CASE(B, G) \
+  if (d->bits == B && d->group == G) return launch_lut_a8_t<B, QX_CODEBOOK, G>(d, packed, x, y, s);
+  QX_LUT_A8_CASE(3, 32) QX_LUT_A8_CASE(3, 64) QX_LUT_A8_CASE(3, 128)
+  QX_LUT_A8_CASE(4, 32) QX_LUT_A8_CASE(4, 64) QX_LUT_A8_CASE(4, 128)
+#undef QX_LUT_A8_CASE
+  return QX_E_UNSUPPORTED;
 }
 
 }  // namespace qx

@@ -203,7 +203,7 @@ int qx_gemv_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t
                hipStream_t stream) {
   const int st = check_desc(d);
   if (st != QX_OK) return st;
-  if ((d->kind != QX_UNIFORM && d->kind != QX_Q4X) || d->k > 88 * 128) return QX_E_UNSUPPORTED;
+  if (d->k > 88 * 128) return QX_E_UNSUPPORTED;
   if (d->n == 0) return QX_OK;
   if (packed == nullptr || x == nullptr || y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(x) || !aligned2(y)) return QX_E_ARG;

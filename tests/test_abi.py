@@ -236,11 +236,12 @@ def test_q4x_device_calls_reject_before_launch():
 def test_gemv_a8_rejects_before_launch():
     lib = qx.load()
     P = ctypes.c_void_p
-    d = qx.desc(4, 128, 3, 128, qx.QX_CODEBOOK)
-    assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
-    q4 = qx.desc(4, 128, 4, 64, qx.QX_Q4X)  # supported: only argument errors are checked here
-    assert lib.qx_gemv_a8(ctypes.byref(q4), None, P(16), P(16), None) == qx.QX_E_ARG
-    for long_k in (qx.desc(4, 89 * 128, 4, 128, qx.QX_UNIFORM), qx.desc(4, 89 * 128, 4, 64, qx.QX_Q4X)):
+    for kind, bits, group in ((qx.QX_CODEBOOK, 3, 128), (qx.QX_Q4X, 4, 64)):
+        d = qx.desc(4, 128, bits, group, kind)  # supported: only argument errors are checked here
+        assert lib.qx_gemv_a8(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
+        assert lib.qx_gemv_a8(ctypes.byref(d), P(16), P(24), P(16), None) == qx.QX_E_ARG
+    for long_k in (qx.desc(4, 89 * 128, 4, 128, qx.QX_UNIFORM), qx.desc(4, 89 * 128, 4, 64, qx.QX_Q4X),
+                   qx.desc(4, 89 * 128, 3, 64, qx.QX_CODEBOOK)):
         assert lib.qx_gemv_a8(ctypes.byref(long_k), P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
     d = qx.desc(4, 128, 4, 128, qx.QX_UNIFORM)
     assert lib.qx_gemv_a8(ctypes.byref(d), None, P(16), P(16), None) == qx.QX_E_ARG
