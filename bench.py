@@ -17,7 +17,8 @@ Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
 --workload batch (the same decode step for 1 to 4 sequences decoded together,
 one line per batch size), --workload c5 (prefill GEMM, m = 16, 64, 512), --workload c5a8 (the same with int8
-per-token activations), --workload q4x (the paper's Q4X
+per-token activations), --workload q4xgemm (the same MLP prefill in the Q4X format, fp16 and int8
+activations), --workload q4x (the paper's Q4X
 format on the MLP shapes gate 11008x4096 and down 4096x11008, one line each,
 rotated over copies like c1-c3), --workload a8 (c1, c2, c3, the 22016x4096 gate|up
 matrix and the Q4X gate matrix with fp16 and with int8 activations, one line each), --workload tp8
@@ -44,7 +45,7 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, published
 FP16_MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 matrix-core peak, published
 INT8_MFMA_PEAK_TOPS = 5000.0    # dense int8 matrix-core peak, published
 METRIC = "batch-1 qGEMV effective HBM GB/s (% of peak) + µs per 7B decode step"
-KERNEL_SOURCES = ["qx_device.h", "gemv_common.h", "gemv.hip", "gemm.hip", "dequant.hip"]
+KERNEL_SOURCES = ["qx_device.h", "gemv_common.h", "gemv.hip"]  # what the measured GEMV kernel is built from
 
 
 def log(msg: str) -> None:
@@ -463,13 +464,20 @@ def bench_single_gemv(args, qx, name, a8=False):
                          "avg_launch_us": round(ms * 1e3, 3)}}
 
 
-def bench_gemm(args, qx, a8=False):
+def bench_gemm(args, qx, a8=False, q4x=False):
     """c5 prefill: gate, up, down at m = 16, 64, 512. a8: activations quantized per token
-    (qx_quantize_a8, once per input, inside the timed region) and qx_gemm_a8."""
+    (qx_quantize_a8, once per input, inside the timed region) and qx_gemm_a8. q4x: the same
+    MLP shapes in the paper's Q4X format (Table 2 runs Q4X prefill with 8-bit activations)."""
     import torch
     from qx_inputs import configs
     dev = torch.device("cuda:0")
-    mats = {nm: quantize_and_pack(configs.c5_matrix(nm), qx, dev) for nm in ("gate", "up", "down")}
+    if q4x:
+        specs = {"gate": configs.q4x_matrix("gate"), "down": configs.q4x_matrix("down"),
+                 "up": configs.MatrixSpec("q4x.up", configs.MLP, configs.HIDDEN, "t4", configs.T4_STD,
+                                          5, 2, 4, 64, configs.Q4X)}
+    else:
+        specs = {nm: configs.c5_matrix(nm) for nm in ("gate", "up", "down")}
+    mats = {nm: quantize_and_pack(specs[nm], qx, dev) for nm in ("gate", "up", "down")}
     # distinct copies of the three matrices, >= 512 MB in all, so that the codes of one
     # set are not still in the 256 MB last-level cache when they are read again
     set_bytes = sum(mats[nm].nbytes for nm in mats)
@@ -497,20 +505,22 @@ def bench_gemm(args, qx, a8=False):
         # ms for the three GEMMs
         t = time_graph(launch_all, torch.cuda.Stream(), 3, 1) / nsets
         flops = 2.0 * m * sum(mats[nm].desc.n * mats[nm].desc.k for nm in mats)
-        byts = sum(configs.c5_matrix(nm).packed_bytes for nm in mats) + m * 90_624
+        byts = sum(specs[nm].packed_bytes for nm in mats) + m * 90_624
         tf = flops / (t * 1e-3) / 1e12
         gbs = byts / (t * 1e-3) / 1e9
-        peak = INT8_MFMA_PEAK_TOPS if a8 else FP16_MFMA_PEAK_TFLOPS
+        int8_cores = a8 and not q4x  # Q4X levels are fp16: its A8 products run on the fp16 matrix cores
+        peak = INT8_MFMA_PEAK_TOPS if int8_cores else FP16_MFMA_PEAK_TFLOPS
         hbm_t, mfma_t = byts / (HBM_PEAK_GBS * 1e9), flops / (peak * 1e12)
         bound = "hbm" if hbm_t >= mfma_t else "mfma"
         frac = (hbm_t if bound == "hbm" else mfma_t) / (t * 1e-3)
-        unit = "TOP/s" if a8 else "TFLOP/s"
-        lines.append({"metric": f"prefill qGEMM{' W·A8' if a8 else ''} (gate+up+down, m={m})",
+        unit = "TOP/s" if int8_cores else "TFLOP/s"
+        fmt_name = "Q4X (4 x 16 matrix codebook, scale + 2-bit selector per group of 64)" if q4x else "3-bit uniform g64"
+        lines.append({"metric": f"prefill qGEMM{' Q4X' if q4x else ''}{' W·A8' if a8 else ''} (gate+up+down, m={m})",
                       "value": round(tf, 3), "unit": unit, "n_gpus": 1, "steps": 3 * nsets,
                       "warmup": nsets, "ms_per_step": round(t, 6), "higher_is_better": True,
-                      "scaling": "weak", "vs_baseline": None, "dtype": "i8" if a8 else "f16",
+                      "scaling": "weak", "vs_baseline": None, "dtype": "i8" if int8_cores else "f16",
                       "data": "synthetic",
-                      "config": {"workload": f"c5 MLP prefill GEMM m={m}, 3-bit uniform g64, "
+                      "config": {"workload": f"{'Q4X ' if q4x else 'c5 '}MLP prefill GEMM m={m}, {fmt_name}, "
                                              + ("int8 per-token activations (quantized in the timed "
                                                 "region), " if a8 else "")
                                              + f"graph over {nsets} copies of the three matrices"},
@@ -588,7 +598,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode7b",
-                    choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "c5a8", "q4x", "a8",
+                    choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "c5a8", "q4x", "q4xgemm", "a8",
                              "tp8", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -626,6 +636,10 @@ def main():
     elif args.workload == "batch":
         for line in bench_decode_batch(args, qx):
             print(json.dumps(line), flush=True)
+    elif args.workload == "q4xgemm":
+        for a8 in (False, True):
+            for line in bench_gemm(args, qx, a8=a8, q4x=True):
+                print(json.dumps(line), flush=True)
     elif args.workload == "c5a8":
         for line in bench_gemm(args, qx, a8=True):
             print(json.dumps(line), flush=True)

@@ -197,13 +197,18 @@ int qx_quantize_a8(int32_t m, int32_t k, const uint16_t* X, int8_t* Xq, float* s
                    hipStream_t stream);
 
 /*
- * qx_gemm_a8 -- Y = X W'^T with 8-bit activations (device; uniform kind).
- * Passage: as qx_gemv_a8, for m activation rows (prefill of a W3A8 model).
+ * qx_gemm_a8 -- Y = X W'^T with 8-bit activations (device; every kind).
+ * Passage: as qx_gemv_a8, for m activation rows (prefill of a W3A8 model; Table 2
+ * runs Q4X prefill with 8-bit activations).
  *   Xq, sx as qx_quantize_a8 wrote them for the same k; Y fp16 [m][n]
- *   (written, 2-byte aligned) = sx[r] * sum_j s_j * sum_{k in group j}
- *   (q - z_j) * xq[r][k], the group sums exact (int8 matrix-core products,
- *   int32 accumulation), scaled in fp32, rounded to nearest-even.
- * Codebook and Q4X descriptors: QX_E_UNSUPPORTED. m = 0 or n = 0 is a no-op.
+ *   (written, 2-byte aligned), rounded to nearest-even:
+ *   uniform: sx[r] * sum_j s_j * sum_{k in group j} (q - z_j) * xq[r][k], the
+ *     group sums exact (int8 matrix-core products, int32 accumulation), scaled
+ *     in fp32;
+ *   codebook and Q4X: sx[r] * sum_k W'[n][k] * xq[r][k] on the fp16 matrix
+ *     cores (W' as qx_dequant gives it, the codes xq as exact fp16 integers,
+ *     fp32 accumulation), scaled in fp32.
+ * m = 0 or n = 0 is a no-op; m must be <= 65536.
  */
 int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq, const float* sx,
                uint16_t* Y, hipStream_t stream);

@@ -213,9 +213,22 @@ __device__ __forceinline__ u32x4 x_piece(u32x2 lo, u32x2 hi) {
   return o;
 }
 
-template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX>
+// Four int8 activation codes (the bytes of b) as exact binary16 pairs (v0, v1), (v2, v3):
+// v + 128 in the fraction bits of 1024, minus 1152.
+__device__ __forceinline__ u32x2 i8x4_to_h4(uint32_t b) {
+  const uint32_t u = b ^ 0x80808080u;
+  const uint32_t m1152 = 0xE480E480u;  // (-1152, -1152)
+  return u32x2{hadd2(perm(0u, u, 0x0C010C00u) | kMagic1024, m1152),
+               hadd2(perm(0u, u, 0x0C030C02u) | kMagic1024, m1152)};
+}
+
+// A8: X holds int8 activation codes [m][k] (qx_quantize_a8) and sx their per-row
+// scales; the codes enter the products as exact binary16 integers and each output
+// row is multiplied by its scale before rounding. Otherwise X is fp16 [m][k].
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8>
 __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restrict__ packed,
-                                                             const uint16_t* __restrict__ X,
+                                                             const void* __restrict__ Xv,
+                                                             const float* __restrict__ sx,
                                                              uint16_t* __restrict__ Y, int n,
                                                              int k, int m, int nx, int my) {
   constexpr int NG = 4 / KS;  // wave groups on different weight rows
@@ -328,9 +341,15 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
       const int c = min(r * KS + kq, C - 1), row = min(m0 + ml, m - 1);
       int o1, o2;
       x_piece_offsets<BITS>(f, o1, o2);
-      const uint16_t* src = X + (size_t)row * k + (size_t)c * 128;
-      lo[i] = *reinterpret_cast<const u32x2*>(src + o1);
-      hi[i] = *reinterpret_cast<const u32x2*>(src + o2);
+      if constexpr (A8) {
+        const int8_t* src = static_cast<const int8_t*>(Xv) + (size_t)row * k + (size_t)c * 128;
+        lo[i] = i8x4_to_h4(*reinterpret_cast<const uint32_t*>(src + o1));
+        hi[i] = i8x4_to_h4(*reinterpret_cast<const uint32_t*>(src + o2));
+      } else {
+        const uint16_t* src = static_cast<const uint16_t*>(Xv) + (size_t)row * k + (size_t)c * 128;
+        lo[i] = *reinterpret_cast<const u32x2*>(src + o1);
+        hi[i] = *reinterpret_cast<const u32x2*>(src + o2);
+      }
     }
   };
   auto store_x = [&](int buf, const u32x2 (&lo)[kXPieces], const u32x2 (&hi)[kXPieces]) {
@@ -452,20 +471,21 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = m0 + 16 * mt + 4 * g + r;
-          if (row < m) Y[(size_t)row * n + col] = (uint16_t)float_to_half_bits(acc[mt][nt][r]);
+          if (row < m)
+            Y[(size_t)row * n + col] = (uint16_t)float_to_half_bits(A8 ? acc[mt][nt][r] * sx[row] : acc[mt][nt][r]);
         }
     }
   }
 }
 
-template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX>
-static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y,
-                            hipStream_t s) {
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8>
+static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* X, const float* sx,
+                            uint16_t* Y, hipStream_t s) {
   constexpr int BN = 16 * NT * (4 / KS), BM = 16 * MT;
   const int nx = (d->n + BN - 1) / BN, my = (m + BM - 1) / BM;
   const unsigned blocks = my == 1 ? (unsigned)nx : (unsigned)((nx + 7) / 8) * 8u * (unsigned)my;
-  hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, MT, NT, KS, S, DX>), dim3(blocks), dim3(kGemmThreads),
-                     0, s, p, X, Y, d->n, d->k, m, nx, my);
+  hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, MT, NT, KS, S, DX, A8>), dim3(blocks), dim3(kGemmThreads),
+                     0, s, p, X, sx, Y, d->n, d->k, m, nx, my);
 }
 
 // Tile shape per activation row count (from a sweep of MT, NT, KS, S, DX on the
@@ -480,39 +500,39 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const uint16
 #ifndef QX_GEMM_CFG
 #define QX_GEMM_CFG 0  // 0: by m; 1, 2, 4 force one shape
 #endif
-template <int BITS, int KIND, int G>
-static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint16_t* X,
+template <int BITS, int KIND, int G, bool A8 = false>
+static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void* X, const float* sx,
                          uint16_t* Y, hipStream_t s) {
   const char* p = static_cast<const char*>(packed);
   constexpr bool kUni = KIND == QX_UNIFORM;
   const int cfg = QX_GEMM_CFG > 0 ? QX_GEMM_CFG : m <= 16 ? 1 : m <= 64 ? 2 : 4;
   switch (cfg) {
     case 1:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 2, 2>(d, p, m, X, Y, s);
-      else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1>(d, p, m, X, Y, s);
+      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 2, 2, A8>(d, p, m, X, sx, Y, s);
+      else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
       break;
     case 2:
       if constexpr (kUni) {
         // at most 128 tiles of 32 x 32 (a 4096-row matrix at m <= 32): four waves per tile
         const long tiles = (long)((d->n + 31) / 32) * ((m + 31) / 32);
-        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 1>(d, p, m, X, Y, s);
-        else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1>(d, p, m, X, Y, s);
+        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 1, A8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1, A8>(d, p, m, X, sx, Y, s);
       } else {
-        launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2>(d, p, m, X, Y, s);
+        launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2, A8>(d, p, m, X, sx, Y, s);
       }
       break;
     default:
       if constexpr (kUni) {
         // few 128 x 64 tiles (e.g. 4096 weight rows at m <= 256): split k over the waves
         const long tiles = (long)((d->n + 127) / 128) * ((m + 63) / 64);
-        if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1>(d, p, m, X, Y, s);
-        else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2>(d, p, m, X, Y, s);
-        else launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2>(d, p, m, X, Y, s);
+        if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
+        else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
       } else {
         // codebook and Q4X: 64 x 64 tiles; at most 128 of them split k over two waves
         const long tiles = (long)((d->n + 63) / 64) * ((m + 63) / 64);
-        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 1, 2, 4, 2>(d, p, m, X, Y, s);
-        else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2>(d, p, m, X, Y, s);
+        if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 1, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
       }
       break;
   }
@@ -522,13 +542,26 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const uint
 int launch_gemm(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y,
                 hipStream_t s) {
 #define QX_GEMM_CASE(B, K, G) \
-  if (d->bits == B && d->kind == K && d->group == G) return launch_gemm_t<B, K, G>(d, packed, m, X, Y, s);
+  if (d->bits == B && d->kind == K && d->group == G) return launch_gemm_t<B, K, G>(d, packed, m, X, nullptr, Y, s);
   QX_GEMM_CASE(3, 0, 32) QX_GEMM_CASE(3, 0, 64) QX_GEMM_CASE(3, 0, 128)
   QX_GEMM_CASE(3, 1, 32) QX_GEMM_CASE(3, 1, 64) QX_GEMM_CASE(3, 1, 128)
   QX_GEMM_CASE(4, 0, 32) QX_GEMM_CASE(4, 0, 64) QX_GEMM_CASE(4, 0, 128)
   QX_GEMM_CASE(4, 1, 32) QX_GEMM_CASE(4, 1, 64) QX_GEMM_CASE(4, 1, 128)
   QX_GEMM_CASE(4, 2, 64)
 #undef QX_GEMM_CASE
+  return QX_E_UNSUPPORTED;
+}
+
+// Codebook and Q4X weights with int8 activation rows (qx_gemm_a8): the fp16 matrix-core
+// GEMM above on the activation codes, scaled per row.
+int launch_gemm_lut_a8(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx,
+                       uint16_t* Y, hipStream_t s) {
+#define QX_GEMM_A8_CASE(B, K, G) \
+  if (d->bits == B && d->kind == K && d->group == G) return launch_gemm_t<B, K, G, true>(d, packed, m, Xq, sx, Y, s);
+  QX_GEMM_A8_CASE(3, 1, 32) QX_GEMM_A8_CASE(3, 1, 64) QX_GEMM_A8_CASE(3, 1, 128)
+  QX_GEMM_A8_CASE(4, 1, 32) QX_GEMM_A8_CASE(4, 1, 64) QX_GEMM_A8_CASE(4, 1, 128)
+  QX_GEMM_A8_CASE(4, 2, 64)
+#undef QX_GEMM_A8_CASE
   return QX_E_UNSUPPORTED;
 }
 

@@ -223,11 +223,12 @@ int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq
   const int st = check_desc(d);
   if (st != QX_OK) return st;
   if (m < 0 || m > 65536) return QX_E_ARG;
-  if (d->kind != QX_UNIFORM) return QX_E_UNSUPPORTED;
   if (m == 0 || d->n == 0) return QX_OK;
   if (packed == nullptr || Xq == nullptr || sx == nullptr || Y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(Xq) || (reinterpret_cast<uintptr_t>(sx) & 3u) != 0 || !aligned2(Y))
     return QX_E_ARG;
+  if (d->kind != QX_UNIFORM)  // table levels are fp16: the fp16 matrix cores on the int8 codes
+    return qx::launch_gemm_lut_a8(d, packed, m, Xq, sx, Y, stream);
   if (m == 1 && d->k <= 88 * 128)  // one row: the A8 GEMV (v_dot4 on its staged int8 row)
     return qx::launch_gemv_a8q(d, packed, Xq, sx, Y, stream);
   // a few rows: every code decoded once for all of them, where that measured faster

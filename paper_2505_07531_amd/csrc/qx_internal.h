@@ -45,6 +45,8 @@ int launch_gemv_a8_multi(const qx_desc* d, const void* packed, int m, const int8
                          uint16_t* Y, hipStream_t s);
 // The A8 GEMV of Q4X matrices (fp16 table entries times the integer xq; k <= 88*128).
 int launch_gemv_lut_a8(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y, hipStream_t s);
+int launch_gemm_lut_a8(const qx_desc* d, const void* packed, int m, const int8_t* Xq, const float* sx,
+                       uint16_t* Y, hipStream_t s);
 // The A8 GEMV on one row already quantized (k <= 88*128).
 int launch_gemv_a8q(const qx_desc* d, const void* packed, const int8_t* xq, const float* sx, uint16_t* y,
                     hipStream_t s);

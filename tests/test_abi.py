@@ -261,8 +261,9 @@ def test_a8_gemm_calls_reject_before_launch():
     assert lib.qx_quantize_a8(4, 4096, P(16), P(16), P(18), None) == qx.QX_E_ARG  # sx alignment
     assert lib.qx_quantize_a8(0, 4096, None, None, None, None) == qx.QX_OK
     for kind, bits, group in ((qx.QX_CODEBOOK, 3, 128), (qx.QX_Q4X, 4, 64)):
-        bad = qx.desc(64, 4096, bits, group, kind)
-        assert lib.qx_gemm_a8(ctypes.byref(bad), P(16), 4, P(16), P(16), P(16), None) == qx.QX_E_UNSUPPORTED
+        t = qx.desc(64, 4096, bits, group, kind)  # supported: only argument errors are checked here
+        assert lib.qx_gemm_a8(ctypes.byref(t), None, 4, P(16), P(16), P(16), None) == qx.QX_E_ARG
+        assert lib.qx_gemm_a8(ctypes.byref(t), P(16), 4, P(16), P(18), P(16), None) == qx.QX_E_ARG
     assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 4, None, P(16), P(16), None) == qx.QX_E_ARG
     assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 4, P(16), P(16), P(17), None) == qx.QX_E_ARG
     assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 65537, P(16), P(16), P(16), None) == qx.QX_E_ARG

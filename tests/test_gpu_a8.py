@@ -221,3 +221,38 @@ def test_codebook_gemv_a8_matches_oracle(gpu, fmt, shape):
     assert oracle.normwise_rel_err(y, ref) <= TOL
     assert np.array_equal(y.view(np.uint16), pw.gemv_a8(to_dev(x)).cpu().numpy().view(np.uint16))
     assert not np.any(pw.gemv_a8(to_dev(np.zeros(k, np.float16))).cpu().numpy())
+
+
+@pytest.mark.parametrize("fmt", [(3, 1, 128), (3, 1, 32), (4, 1, 64), (4, 2, 64)],
+                         ids=lambda f: f"b{f[0]}k{f[1]}g{f[2]}")
+@pytest.mark.parametrize("shape", [(1, 130, 4096), (3, 300, 1152), (16, 257, 11008), (70, 1000, 2048),
+                                   (256, 4096, 1024)], ids=lambda s: f"m{s[0]}_{s[1]}x{s[2]}")
+def test_table_gemm_a8_matches_oracle(gpu, fmt, shape):
+    """qx_gemm_a8 on codebook and Q4X weights: the int8 codes of qx_quantize_a8 times W' on the
+    fp16 matrix cores, scaled per row, against the per-row oracle of the same quantization (W'
+    rounded to binary16 for Q4X, as qx_dequant gives it: within the normwise bound)."""
+    import torch
+    qx = gpu
+    bits, kind, g = fmt
+    m, n, k = shape
+    print(f"table a8 gemm {fmt} {shape}", flush=True)
+    if kind == qx.QX_Q4X:
+        from qx_inputs import q4x as qq
+        q = qq.quantize_q4x(qi.weights("t4", 0.0141421, n + k, 0, n, k))
+    else:
+        q = realistic_quant(n, k, bits, g, kind, seed=n + k + m)
+    X = activations(k, seed=k + m, m=m)
+    pw = qx.PackedWeight.from_quant(q, device="cuda")
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = pw.gemm_a8(Xq, sx).cpu().numpy()
+    for r in range(m):
+        if kind == qx.QX_Q4X:
+            ref = a8.gemv_a8_q4x(q.codes, q.scales, q.selectors, q.codebook, X[r])
+        else:
+            ref = a8.gemv_a8_codebook(q.codes, g, q.codebook, X[r])
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
+    Y2 = pw.gemm_a8(Xq, sx).cpu().numpy()
+    assert np.array_equal(Y.view(np.uint16), Y2.view(np.uint16))
+    if m > 1:  # a row is the same product whatever else is in the batch
+        y0 = pw.gemm_a8(Xq[:1].contiguous(), sx[:1].contiguous()).cpu().numpy()
+        assert oracle.normwise_rel_err(y0[0], Y[0].astype(np.float64)) <= TOL
