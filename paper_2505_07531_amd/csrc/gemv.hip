@@ -245,35 +245,6 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
 #define QX_GEMV_WPB 4  // waves per block of the wave kernel
 #endif
 
-// Rows per block and block size of the row kernel for C chunks per row: among
-// blocks of at least 256 threads (x is staged once per block), the R whose R*C
-// items leave the fewest idle lanes in 64*ceil(R*C/64) threads; at most 8 rows
-// when rows are long. Short rows (< 32 chunks) take at most n / QX_ROW_MIN_BLOCKS
-// rows, so that the grid has blocks for every compute unit where n allows (4096
-// rows of 4 chunks: 64 blocks of 64 rows 5.3 us, 512 blocks of 8 rows 3.9 us; 4096
-// rows of 11 chunks 4.9 vs 3.6 us), but at least 4 above 16 chunks (x in at most 4
-// pieces per thread) and not for heavy items (codebook-4 g32, measured slower).
-#ifndef QX_ROW_MIN_BLOCKS
-#define QX_ROW_MIN_BLOCKS 512
-#endif
-static void gemv_row_shape(int n, int C, bool heavy_items, int* R, int* threads) {
-  int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
-  if (QX_ROW_MIN_BLOCKS > 0 && !heavy_items && C < 32)
-    r_max = std::max(std::min(C > 16 ? 4 : 1, r_max), std::min(r_max, n / QX_ROW_MIN_BLOCKS));
-  int best_r = 0;
-  double best_u = -1.0;
-  for (int pass = 0; pass < 2 && best_r == 0; ++pass) {
-    for (int r = 1; r <= r_max; ++r) {
-      const int t = 64 * ((r * C + 63) / 64);
-      if ((pass == 0 && t < 256) || (C < 32 && t < 4 * C)) continue;  // short rows: x in <= 4 pieces per thread
-      const double u = (double)(r * C) / t;
-      if (u > best_u + 1e-9) { best_u = u; best_r = r; }
-    }
-  }
-  *R = best_r;
-  *threads = 64 * ((best_r * C + 63) / 64);
-}
-
 static void gemv_tile_shape(int n, int k, int* R, int* items) {
   const int C = k / 128;
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;

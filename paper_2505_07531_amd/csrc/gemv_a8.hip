@@ -13,7 +13,7 @@
 // code costs about a quarter of the VALU work of the fp16-activation path. The
 // launch paths follow the fp16 GEMV: one 128-code chunk per lane, a wave per row
 // pair for k = 128*32 or 128*64, rows of up to 88 chunks split over a block.
-#include "qx_device.h"
+#include "gemv_common.h"  // also the row kernels' shape rule
 #include "qx_internal.h"
 
 #include <algorithm>
@@ -353,23 +353,6 @@ __global__ __launch_bounds__(512) void gemv_a8_multi_kernel(const char* __restri
   }
 }
 
-// Rows per block for the row kernel: the R (at most 8 for long rows) whose R*C items
-// leave the fewest idle lanes in blocks of at least 256 threads.
-void a8_row_shape(int C, int* R, int* threads) {
-  const int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
-  int best_r = 1;
-  double best_u = -1.0;
-  for (int pass = 0; pass < 2 && best_u < 0; ++pass)
-    for (int r = 1; r <= r_max; ++r) {
-      const int th = 64 * ((r * C + 63) / 64);
-      if (pass == 0 && th < 256) continue;
-      const double u = (double)(r * C) / th;
-      if (u > best_u + 1e-9) { best_u = u; best_r = r; }
-    }
-  *R = best_r;
-  *threads = 64 * ((best_r * C + 63) / 64);
-}
-
 template <int BITS, int G, bool PREQ>
 int launch_gemv_a8_t(const qx_desc* d, const void* packed, const void* x, const float* sx, uint16_t* y,
                      hipStream_t s) {
@@ -385,7 +368,7 @@ int launch_gemv_a8_t(const qx_desc* d, const void* packed, const void* x, const 
       hipLaunchKernelGGL((gemv_a8_wave_kernel<BITS, G, 64, WPB, PREQ>), grid, block, 0, s, p, x, sx, y, d->n);
   } else if (C <= 88) {
     int R, threads;
-    a8_row_shape(C, &R, &threads);
+    gemv_row_shape(d->n, C, false, &R, &threads);
     const size_t lds = (size_t)C * kX8Block + (size_t)(R * C + C * (128 / G)) * sizeof(float);
     const int xp = (C * 16 + threads - 1) / threads;
     const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);

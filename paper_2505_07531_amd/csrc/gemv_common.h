@@ -316,6 +316,39 @@ __device__ __forceinline__ void stage_q4x_lut(const char* __restrict__ packed, i
   stage_q4x_tables(packed + q4x_offsets(n, k).codebook, lut);
 }
 
+// Rows per block R and block size of the row kernels (one (row, chunk) item per
+// lane, x staged once per block) for n rows of C chunks: among blocks of at least
+// 256 threads, the R whose R*C items leave the fewest idle lanes in 64*ceil(R*C/64)
+// threads; at most 8 rows when rows are long. Short rows (< 32 chunks) take at most
+// n / QX_ROW_MIN_BLOCKS rows, so that the grid has blocks for every compute unit
+// where n allows (4096 rows of 4 chunks: 64 blocks of 64 rows 5.3 us, 512 blocks of 8
+// rows 3.9 us; 4096 rows of 11 chunks 4.9 vs 3.6 us), but at least 4 above 16
+// chunks, and x stays within 4 pieces per thread; heavy items (codebook-4 g32,
+// measured slower) keep the rule without that cap.
+#ifndef QX_ROW_MIN_BLOCKS
+#define QX_ROW_MIN_BLOCKS 512
+#endif
+inline void gemv_row_shape(int n, int C, bool heavy_items, int* R, int* threads) {
+  int r_max = C >= 32 ? (8 < 1024 / C ? 8 : 1024 / C) : (256 < 1024 / C ? 256 : 1024 / C);
+  if (QX_ROW_MIN_BLOCKS > 0 && !heavy_items && C < 32) {
+    const int floor_r = (C > 16 ? 4 : 1) < r_max ? (C > 16 ? 4 : 1) : r_max;
+    const int cap = r_max < n / QX_ROW_MIN_BLOCKS ? r_max : n / QX_ROW_MIN_BLOCKS;
+    r_max = floor_r > cap ? floor_r : cap;
+  }
+  int best_r = 0;
+  double best_u = -1.0;
+  for (int pass = 0; pass < 2 && best_r == 0; ++pass) {
+    for (int r = 1; r <= r_max; ++r) {
+      const int t = 64 * ((r * C + 63) / 64);
+      if ((pass == 0 && t < 256) || (C < 32 && t < 4 * C)) continue;  // short rows: x in <= 4 pieces per thread
+      const double u = (double)(r * C) / t;
+      if (u > best_u + 1e-9) { best_u = u; best_r = r; }
+    }
+  }
+  *R = best_r;
+  *threads = 64 * ((best_r * C + 63) / 64);
+}
+
 // Byte offset of the group sums after C chunks of x and n floats of partials.
 __host__ __device__ constexpr int row_lds_gsum_offset(int C, int nfloats) {
   return C * kXBlock + (nfloats * 4 + 7) / 8 * 8;

@@ -154,19 +154,8 @@ static int launch_lut_a8_t(const qx_desc* d, const void* packed, const uint16_t*
       hipLaunchKernelGGL((gemv_lut_a8_wave_kernel<BITS, KIND, G, 64, WPB>), grid, block, 0, s, p, x, y, d->n);
     return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
   }
-  // R rows per block: the R (at most 8 for long rows) whose R*C items leave the fewest
-  // idle lanes in blocks of at least 256 threads
-  const int r_max = C >= 32 ? std::min(8, 1024 / C) : std::min(256, 1024 / C);
-  int R = 1;
-  double best_u = -1.0;
-  for (int pass = 0; pass < 2 && best_u < 0; ++pass)
-    for (int r = 1; r <= r_max; ++r) {
-      const int th = 64 * ((r * C + 63) / 64);
-      if (pass == 0 && th < 256) continue;
-      const double u = (double)(r * C) / th;
-      if (u > best_u + 1e-9) { best_u = u; R = r; }
-    }
-  const int threads = 64 * ((R * C + 63) / 64);
+  int R, threads;
+  gemv_row_shape(d->n, C, KIND == QX_CODEBOOK && BITS == 4 && G == 32, &R, &threads);
   const size_t lds = (size_t)C * kXBlock + (size_t)R * C * sizeof(float);
   const int xp = (C * 16 + threads - 1) / threads;
   const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
@@ -174,7 +163,7 @@ static int launch_lut_a8_t(const qx_desc* d, const void* packed, const uint16_t*
     hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 1>), grid, block, lds, s, p, x, y, d->n, d->k, R);
   else if (xp <= 2)
     hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 2>), grid, block, lds, s, p, x, y, d->n, d->k, R);
-  else  // blocks have >= 256 threads or C < 32, so xp <= ceil(88*16/256) = 6
+  else  // long rows have blocks of >= 256 threads, so xp <= ceil(88*16/256) = 6
     hipLaunchKernelGGL((gemv_lut_a8_row_kernel<BITS, KIND, G, 6>), grid, block, lds, s, p, x, y, d->n, d->k, R);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
