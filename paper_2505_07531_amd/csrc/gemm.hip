@@ -225,22 +225,24 @@ __device__ __forceinline__ u32x2 i8x4_to_h4(uint32_t b) {
 // A8: X holds int8 activation codes [m][k] (qx_quantize_a8) and sx their per-row
 // scales; the codes enter the products as exact binary16 integers and each output
 // row is multiplied by its scale before rounding. Otherwise X is fp16 [m][k].
-template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8>
-__global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restrict__ packed,
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8, int W = 4>
+__global__ __launch_bounds__(64 * W) void gemm_kernel(const char* __restrict__ packed,
                                                              const void* __restrict__ Xv,
                                                              const float* __restrict__ sx,
                                                              uint16_t* __restrict__ Y, int n,
                                                              int k, int m, int nx, int my) {
-  constexpr int NG = 4 / KS;  // wave groups on different weight rows
+  constexpr int NTH = 64 * W;   // threads per block
+  constexpr int NG = W / KS;  // wave groups on different weight rows
+  static_assert(W % KS == 0, "the k split divides the waves");
   constexpr int BM = 16 * MT, BN = 16 * NT * NG, SC = S * KS;
   using CT = CodeTile<BITS, KIND, G, SC>;
-  constexpr int kXPieces = KS * BM * 16 / kGemmThreads;  // activation pieces per thread and round
+  constexpr int kXPieces = KS * BM * 16 / NTH;  // activation pieces per thread and round
   constexpr int kXBuf = KS * BM * kXRowBytes;
   constexpr int kCTotal = BN * BITS * SC;                                 // 16-byte code pieces
-  constexpr int kCPieces = (kCTotal + kGemmThreads - 1) / kGemmThreads;  // per thread
+  constexpr int kCPieces = (kCTotal + NTH - 1) / NTH;  // per thread
   constexpr int kMetaUnit = KIND == QX_UNIFORM ? 4 : KIND == QX_Q4X ? 8 : 16;  // bytes per table load
-  constexpr int kMPieces = (BN * CT::kMetaRow / kMetaUnit + kGemmThreads - 1) / kGemmThreads;
-  static_assert(KS * BM * 16 % kGemmThreads == 0, "activation pieces must divide evenly");
+  constexpr int kMPieces = (BN * CT::kMetaRow / kMetaUnit + NTH - 1) / NTH;
+  static_assert(KS * BM * 16 % NTH == 0, "activation pieces must divide evenly");
   static_assert(S % DX == 0, "activation register sets must divide the super-round");
   static_assert((KS - 1) * NG * MT * NT * 1024 <= 2 * kXBuf, "reduction must fit the LDS buffers");
   __shared__ __align__(16) char xs[2 * kXBuf];
@@ -276,7 +278,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   auto load_codes = [&](int j, u32x4 (&cr)[kCPieces], u32x4 (&mr)[kMPieces]) {
 #pragma unroll
     for (int i = 0; i < kCPieces; ++i) {
-      const int p = min((int)threadIdx.x + i * kGemmThreads, kCTotal - 1);
+      const int p = min((int)threadIdx.x + i * NTH, kCTotal - 1);
       const int cl = p % SC, sl = (p / SC) % BITS, rl = p / (SC * BITS);
       const int row = min(n0 + rl, n - 1), c = min(j * SC + cl, C - 1);
       cr[i] = *reinterpret_cast<const u32x4*>(packed + (((size_t)row * BITS + sl) * C + c) * 16);
@@ -284,16 +286,16 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
     constexpr int kUnits = CT::kMetaRow / kMetaUnit;  // per row
 #pragma unroll
     for (int i = 0; i < kMPieces; ++i) {
-      const int p = min((int)threadIdx.x + i * kGemmThreads, BN * kUnits - 1);
+      const int p = min((int)threadIdx.x + i * NTH, BN * kUnits - 1);
       const int ul = p % kUnits, rl = p / kUnits;
       const int row = min(n0 + rl, n - 1);
       if constexpr (KIND == QX_Q4X) {
         // chunk c of the row: the scales of groups 2c, 2c + 1 (one dword) and their
         // selectors (4 bits of the row's selector word for groups 16(c/8) ..)
-        const int c = min(j * SC + ul, C - 1), W = (G_row + 15) / 16;
+        const int c = min(j * SC + ul, C - 1), sel_words = (G_row + 15) / 16;
         const uint32_t sc = *reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + 2 * c) * 2);
         const uint32_t sw = *reinterpret_cast<const uint32_t*>(packed + meta_off + meta_off / 16 +
-                                                               ((size_t)row * W + c / 8) * 4);
+                                                               ((size_t)row * sel_words + c / 8) * 4);
         mr[i] = u32x4{sc, (sw >> (4 * (c % 8))) & 0xFu, 0u, 0u};
         continue;
       }
@@ -310,15 +312,15 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   auto store_codes = [&](const u32x4 (&cr)[kCPieces], const u32x4 (&mr)[kMPieces]) {
 #pragma unroll
     for (int i = 0; i < kCPieces; ++i) {
-      const int p = threadIdx.x + i * kGemmThreads;
+      const int p = threadIdx.x + i * NTH;
       const int cl = p % SC, sl = (p / SC) % BITS, rl = p / (SC * BITS);
-      if (kCTotal % kGemmThreads == 0 || p < kCTotal)
+      if (kCTotal % NTH == 0 || p < kCTotal)
         *reinterpret_cast<u32x4*>(cts + rl * CT::kRowStride + sl * SC * 16 + cl * 16) = cr[i];
     }
     constexpr int kUnits = CT::kMetaRow / kMetaUnit;
 #pragma unroll
     for (int i = 0; i < kMPieces; ++i) {
-      const int p = threadIdx.x + i * kGemmThreads;
+      const int p = threadIdx.x + i * NTH;
       if (p < BN * kUnits) {
         const int ul = p % kUnits, rl = p / kUnits;
         char* dst = mts + rl * CT::kMetaStride + ul * kMetaUnit;
@@ -336,7 +338,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   auto load_x = [&](int r, u32x2 (&lo)[kXPieces], u32x2 (&hi)[kXPieces]) {
 #pragma unroll
     for (int i = 0; i < kXPieces; ++i) {
-      const int p = threadIdx.x + i * kGemmThreads;
+      const int p = threadIdx.x + i * NTH;
       const int f = p & 15, ml = (p >> 4) % BM, kq = p / (16 * BM);
       const int c = min(r * KS + kq, C - 1), row = min(m0 + ml, m - 1);
       int o1, o2;
@@ -355,7 +357,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   auto store_x = [&](int buf, const u32x2 (&lo)[kXPieces], const u32x2 (&hi)[kXPieces]) {
 #pragma unroll
     for (int i = 0; i < kXPieces; ++i) {
-      const int p = threadIdx.x + i * kGemmThreads;
+      const int p = threadIdx.x + i * NTH;
       const int f = p & 15, ml = (p >> 4) % BM, kq = p / (16 * BM);
       *reinterpret_cast<u32x4*>(xs + buf * kXBuf + (kq * BM + ml) * kXRowBytes + 16 * f) =
           x_piece<BITS>(lo[i], hi[i]);
@@ -478,13 +480,13 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(const char* __restri
   }
 }
 
-template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8>
+template <int BITS, int KIND, int G, int MT, int NT, int KS, int S, int DX, bool A8, int W = 4>
 static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* X, const float* sx,
                             uint16_t* Y, hipStream_t s) {
-  constexpr int BN = 16 * NT * (4 / KS), BM = 16 * MT;
+  constexpr int BN = 16 * NT * (W / KS), BM = 16 * MT;
   const int nx = (d->n + BN - 1) / BN, my = (m + BM - 1) / BM;
   const unsigned blocks = my == 1 ? (unsigned)nx : (unsigned)((nx + 7) / 8) * 8u * (unsigned)my;
-  hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, MT, NT, KS, S, DX, A8>), dim3(blocks), dim3(kGemmThreads),
+  hipLaunchKernelGGL((gemm_kernel<BITS, KIND, G, MT, NT, KS, S, DX, A8, W>), dim3(blocks), dim3(64 * W),
                      0, s, p, X, sx, Y, d->n, d->k, m, nx, my);
 }
 
@@ -500,6 +502,9 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* 
 #ifndef QX_GEMM_CFG
 #define QX_GEMM_CFG 0  // 0: by m; 1, 2, 4 force one shape
 #endif
+#ifndef QX_GEMM_SMALL_W
+#define QX_GEMM_SMALL_W 4  // 4: waves per block for m <= 16 by shape; 8, 16 force (sweeps)
+#endif
 template <int BITS, int KIND, int G, bool A8 = false>
 static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void* X, const float* sx,
                          uint16_t* Y, hipStream_t s) {
@@ -507,10 +512,24 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
   constexpr bool kUni = KIND == QX_UNIFORM;
   const int cfg = QX_GEMM_CFG > 0 ? QX_GEMM_CFG : m <= 16 ? 1 : m <= 64 ? 2 : 4;
   switch (cfg) {
-    case 1:
-      if constexpr (kUni) launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 2, 2, A8>(d, p, m, X, sx, Y, s);
-      else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
+    case 1: {
+      // rows of more than 64 chunks: the k split over 8 waves (codebook) or 16 (uniform,
+      // m <= 8), each walking fewer chunks; codebook-3 4096x11008 at m = 16 took 24.7 us
+      // with 4 waves and 19.5 with 8, uniform-3 at m = 8 18.2 and 16.1 with 16 (shorter
+      // rows were slower split wider)
+      const int C = d->k / 128;
+      const int w = QX_GEMM_SMALL_W != 4 ? QX_GEMM_SMALL_W
+                    : C > 64 ? (KIND == QX_CODEBOOK ? 8 : kUni && m <= 8 ? 16 : 4) : 4;
+      if constexpr (kUni) {
+        if (w == 16) launch_gemm_cfg<BITS, KIND, G, 1, 1, 16, 1, 1, A8, 16>(d, p, m, X, sx, Y, s);
+        else if (w == 8) launch_gemm_cfg<BITS, KIND, G, 1, 1, 8, 1, 1, A8, 8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 2, 2, A8>(d, p, m, X, sx, Y, s);
+      } else {  // 16 waves do not fit the tables of the codebook formats in LDS
+        if (w >= 8) launch_gemm_cfg<BITS, KIND, G, 1, 1, 8, 1, 1, A8, 8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 1, 1, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
+      }
       break;
+    }
     case 2:
       if constexpr (kUni) {
         // at most 128 tiles of 32 x 32 (a 4096-row matrix at m <= 32): four waves per tile
