@@ -502,6 +502,12 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* 
 #ifndef QX_GEMM_CFG
 #define QX_GEMM_CFG 0  // 0: by m; 1, 2, 4 force one shape
 #endif
+#ifndef QX_GEMM_MID_W
+// rows of more than 64 chunks at 16 < m <= 64: the k split over 8 waves instead of 4
+// (4096x11008 at m = 64: uniform-3 39.9 -> 33.4 us, uniform-4 37.1 -> 29.1, codebook-3
+// 34.8 -> 31.3); 4 keeps the 4-wave shape
+#define QX_GEMM_MID_W 8
+#endif
 #ifndef QX_GEMM_SMALL_W
 #define QX_GEMM_SMALL_W 4  // 4: waves per block for m <= 16 by shape; 8, 16 force (sweeps)
 #endif
@@ -535,9 +541,11 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
         // at most 128 tiles of 32 x 32 (a 4096-row matrix at m <= 32): four waves per tile
         const long tiles = (long)((d->n + 31) / 32) * ((m + 31) / 32);
         if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 1, A8>(d, p, m, X, sx, Y, s);
+        else if (QX_GEMM_MID_W == 8 && d->k > 64 * 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 1, A8, 8>(d, p, m, X, sx, Y, s);
         else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 1, A8>(d, p, m, X, sx, Y, s);
       } else {
-        launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2, A8>(d, p, m, X, sx, Y, s);
+        if (QX_GEMM_MID_W == 8 && d->k > 64 * 128) launch_gemm_cfg<BITS, KIND, G, 2, 1, 4, 2, 2, A8, 8>(d, p, m, X, sx, Y, s);
+        else launch_gemm_cfg<BITS, KIND, G, 2, 1, 2, 2, 2, A8>(d, p, m, X, sx, Y, s);
       }
       break;
     default:

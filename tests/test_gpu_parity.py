@@ -246,6 +246,23 @@ def test_gemm_rows_equal_gemv_within_tolerance(gpu):
         assert oracle.normwise_rel_err(Y[r], y.astype(np.float64)) <= 2 * TOL
 
 
+@pytest.mark.parametrize("fmt", [(3, 0, 64), (4, 0, 128), (3, 1, 128), (4, 1, 32)], ids=_fmt_id)
+@pytest.mark.parametrize("m", [33, 64])
+def test_gemm_long_rows_mid_m(gpu, fmt, m):
+    """Rows of more than 64 chunks at 16 < m <= 64, with enough weight rows that uniform
+    32 x 32 tiles number more than 128 (the shape whose k is split over 8 waves)."""
+    qx = gpu
+    bits, kind, g = fmt
+    n, k = 4200, 11008
+    print(f"gemm long rows {fmt} m={m}", flush=True)
+    q = random_quant(n, k, bits, g, kind, seed=m + g)
+    X = activations(k, seed=m + 3, m=m)
+    Y = _pack(qx, q).gemm(to_dev(X)).cpu().numpy()
+    ref = oracle.gemm(X, _ref_w16(q))
+    for r in range(m):
+        assert oracle.normwise_rel_err(Y[r], ref[r]) <= TOL, r
+
+
 # ---- maximum sizes and degenerate inputs
 
 K_MAX = 1 << 20  # largest k the interface accepts
