@@ -508,6 +508,13 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* 
 // 34.8 -> 31.3); 4 keeps the 4-wave shape
 #define QX_GEMM_MID_W 8
 #endif
+#ifndef QX_GEMM_BIG_W
+// m > 64, rows of more than 64 chunks, 129-256 tiles (one block of 8 waves per compute
+// unit): k split over 2 of 8 waves instead of walked by one (4096x11008 at m = 512:
+// uniform-3 122.7 -> 98.4 us, uniform-4 101.2 -> 84.4; codebook-3 at m = 256 78.6 ->
+// 61.8, but 112.7 -> 120.3 at m = 512, 512 tiles); 4 keeps the 4-wave shapes
+#define QX_GEMM_BIG_W 8
+#endif
 #ifndef QX_GEMM_SMALL_W
 #define QX_GEMM_SMALL_W 4  // 4: waves per block for m <= 16 by shape; 8, 16 force (sweeps)
 #endif
@@ -554,12 +561,19 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
         const long tiles = (long)((d->n + 127) / 128) * ((m + 63) / 64);
         if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        else if (QX_GEMM_BIG_W == 8 && d->k > 64 * 128 && tiles <= 256)
+          launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8, 8>(d, p, m, X, sx, Y, s);
         else launch_gemm_cfg<BITS, KIND, G, 4, 2, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
       } else {
         // codebook and Q4X: 64 x 64 tiles; at most 128 of them split k over two waves
         const long tiles = (long)((d->n + 63) / 64) * ((m + 63) / 64);
         if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 1, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
-        else launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        else if (QX_GEMM_BIG_W == 8 && d->k > 64 * 128 && tiles <= 256 && !(BITS == 4 && G == 32)) {
+          if constexpr (!(BITS == 4 && G == 32))  // 32-code tables of 16 entries overflow LDS at 8 waves
+            launch_gemm_cfg<BITS, KIND, G, 4, 1, 2, 4, 2, A8, 8>(d, p, m, X, sx, Y, s);
+        } else {
+          launch_gemm_cfg<BITS, KIND, G, 4, 1, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        }
       }
       break;
   }
