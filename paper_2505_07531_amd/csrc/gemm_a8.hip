@@ -24,6 +24,12 @@ namespace qx {
 namespace {
 
 constexpr int kA8Threads = 256;
+#ifndef QX_A8_WIDE
+// rows of more than 64 chunks take 8-wave blocks with twice the k split, the same weight
+// rows per block (4096x11008 uniform-3 at m = 16 / 64 / 512: 19.9 / 33.1 / 94.9 ->
+// 13.6 / 24.9 / 81.2 us; 11008x4096 unchanged); 0 keeps the 4-wave shapes
+#define QX_A8_WIDE 1
+#endif
 typedef int32_t i4_t __attribute__((ext_vector_type(4)));
 
 // x * inv + 1.5 * 2^23 in one fused multiply-add: its single rounding is the
@@ -107,22 +113,24 @@ __device__ __forceinline__ u32x2 slot_codes(const char* cb, int g) {
   }
 }
 
-template <int BITS, int G, int MT, int KS>
-__global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restrict__ packed,
+template <int BITS, int G, int MT, int KS, int W = 4>
+__global__ __launch_bounds__(64 * W) void gemm_a8_kernel(const char* __restrict__ packed,
                                                              const int8_t* __restrict__ Xq,
                                                              const float* __restrict__ sx,
                                                              uint16_t* __restrict__ Y, int n, int k,
                                                              int m) {
-  constexpr int NW = 4 / KS;                // wave groups on different weight rows
+  constexpr int NTH = 64 * W;
+  constexpr int NW = W / KS;                // wave groups on different weight rows
+  static_assert(W % KS == 0, "the k split divides the waves");
   constexpr int BM = 16 * MT, BN = 16 * NW, NG = 128 / G;
   constexpr int CS = 80;        // LDS bytes per weight row of the code tile (bank-spread rows)
   constexpr int XS = 144;       // LDS bytes per activation row of the activation tile
   constexpr int XPC = KS * BM * 8;   // 16-byte activation pieces per step (KS chunks)
-  constexpr int XP = (XPC + kA8Threads - 1) / kA8Threads;
+  constexpr int XP = (XPC + NTH - 1) / NTH;
   constexpr int CPC = KS * BN * BITS;  // 16-byte code pieces per step
-  constexpr int CP = (CPC + kA8Threads - 1) / kA8Threads;
+  constexpr int CP = (CPC + NTH - 1) / NTH;
   constexpr int MPC = KS * BN * NG;  // group words per step
-  constexpr int MP = (MPC + kA8Threads - 1) / kA8Threads;
+  constexpr int MP = (MPC + NTH - 1) / NTH;
   static_assert((KS - 1) * NW * MT * 1024 <= KS * BM * XS, "the k-split reduction must fit the LDS tile");
   __shared__ __align__(16) char xs[KS * BM * XS];
   __shared__ __align__(16) char cs[KS * BN * CS];
@@ -141,21 +149,21 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
   auto load = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < XP; ++i) {
-      const int p = min(t + i * kA8Threads, XPC - 1);
+      const int p = min(t + i * NTH, XPC - 1);
       const int q = p / (BM * 8), pr = p % (BM * 8);
       const int row = min(m0 + (pr >> 3), m - 1), c = min(c0 + q, C - 1);
       xr[i] = *reinterpret_cast<const u32x4*>(Xq + (size_t)row * k + (size_t)c * 128 + (pr & 7) * 16);
     }
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
-      const int p = min(t + i * kA8Threads, CPC - 1);
+      const int p = min(t + i * NTH, CPC - 1);
       const int q = p / (BN * BITS), pr = p % (BN * BITS);
       const int row = min(n0 + pr / BITS, n - 1), sl = pr % BITS, c = min(c0 + q, C - 1);
       cr[i] = *reinterpret_cast<const u32x4*>(packed + (((size_t)row * BITS + sl) * C + c) * 16);
     }
 #pragma unroll
     for (int i = 0; i < MP; ++i) {
-      const int p = min(t + i * kA8Threads, MPC - 1);
+      const int p = min(t + i * NTH, MPC - 1);
       const int q = p / (BN * NG), pr = p % (BN * NG);
       const int row = min(n0 + pr / NG, n - 1), c = min(c0 + q, C - 1);
       mr[i] = *reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + c * NG + pr % NG) * 4);
@@ -164,18 +172,18 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
   auto store = [&]() {
 #pragma unroll
     for (int i = 0; i < XP; ++i) {
-      const int p = t + i * kA8Threads;
-      if (XPC % kA8Threads == 0 || p < XPC) *reinterpret_cast<u32x4*>(xs + (p >> 3) * XS + (p & 7) * 16) = xr[i];
+      const int p = t + i * NTH;
+      if (XPC % NTH == 0 || p < XPC) *reinterpret_cast<u32x4*>(xs + (p >> 3) * XS + (p & 7) * 16) = xr[i];
     }
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
-      const int p = t + i * kA8Threads;
-      if (CPC % kA8Threads == 0 || p < CPC) *reinterpret_cast<u32x4*>(cs + (p / BITS) * CS + (p % BITS) * 16) = cr[i];
+      const int p = t + i * NTH;
+      if (CPC % NTH == 0 || p < CPC) *reinterpret_cast<u32x4*>(cs + (p / BITS) * CS + (p % BITS) * 16) = cr[i];
     }
 #pragma unroll
     for (int i = 0; i < MP; ++i) {
-      const int p = t + i * kA8Threads;
-      if (MPC % kA8Threads == 0 || p < MPC) ms[p] = mr[i];
+      const int p = t + i * NTH;
+      if (MPC % NTH == 0 || p < MPC) ms[p] = mr[i];
     }
   };
 
@@ -259,12 +267,12 @@ __global__ __launch_bounds__(kA8Threads) void gemm_a8_kernel(const char* __restr
   }
 }
 
-template <int BITS, int G, int MT, int KS>
+template <int BITS, int G, int MT, int KS, int W = 4>
 void launch_a8_cfg(const qx_desc* d, const char* p, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
                    hipStream_t s) {
-  constexpr int BN = 16 * (4 / KS), BM = 16 * MT;
+  constexpr int BN = 16 * (W / KS), BM = 16 * MT;
   const dim3 grid((unsigned)((d->n + BN - 1) / BN), (unsigned)((m + BM - 1) / BM));
-  hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, MT, KS>), grid, dim3(kA8Threads), 0, s, p, Xq, sx, Y, d->n, d->k, m);
+  hipLaunchKernelGGL((gemm_a8_kernel<BITS, G, MT, KS, W>), grid, dim3(64 * W), 0, s, p, Xq, sx, Y, d->n, d->k, m);
 }
 
 // Tiles by m: few activation rows split each weight tile's chunks over the four
@@ -276,11 +284,22 @@ template <int BITS, int G>
 int launch_gemm_a8_t(const qx_desc* d, const char* p, int m, const int8_t* Xq, const float* sx, uint16_t* Y,
                      hipStream_t s) {
   const long tiles64 = (long)((d->n + 63) / 64) * ((m + 63) / 64);
-  if (m <= 16) launch_a8_cfg<BITS, G, 1, 4>(d, p, m, Xq, sx, Y, s);
-  else if (m <= 64) launch_a8_cfg<BITS, G, 2, 2>(d, p, m, Xq, sx, Y, s);
-  else if (tiles64 < 256) launch_a8_cfg<BITS, G, 4, 4>(d, p, m, Xq, sx, Y, s);
-  else if (tiles64 < 512) launch_a8_cfg<BITS, G, 4, 2>(d, p, m, Xq, sx, Y, s);
-  else launch_a8_cfg<BITS, G, 4, 1>(d, p, m, Xq, sx, Y, s);
+  const bool wide = QX_A8_WIDE && d->k > 64 * 128;  // long rows: twice the waves, each walking half the chunks
+  if (m <= 16) {
+    if (wide) launch_a8_cfg<BITS, G, 1, 8, 8>(d, p, m, Xq, sx, Y, s);
+    else launch_a8_cfg<BITS, G, 1, 4>(d, p, m, Xq, sx, Y, s);
+  } else if (m <= 64) {
+    if (wide) launch_a8_cfg<BITS, G, 2, 4, 8>(d, p, m, Xq, sx, Y, s);
+    else launch_a8_cfg<BITS, G, 2, 2>(d, p, m, Xq, sx, Y, s);
+  } else if (tiles64 < 256) {
+    launch_a8_cfg<BITS, G, 4, 4>(d, p, m, Xq, sx, Y, s);
+  } else if (tiles64 < 512) {
+    if (wide) launch_a8_cfg<BITS, G, 4, 4, 8>(d, p, m, Xq, sx, Y, s);
+    else launch_a8_cfg<BITS, G, 4, 2>(d, p, m, Xq, sx, Y, s);
+  } else {
+    if (wide) launch_a8_cfg<BITS, G, 4, 2, 8>(d, p, m, Xq, sx, Y, s);
+    else launch_a8_cfg<BITS, G, 4, 1>(d, p, m, Xq, sx, Y, s);
+  }
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 

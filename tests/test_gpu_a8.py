@@ -118,6 +118,27 @@ def test_gemm_a8_matches_oracle(gpu, fmt, m, n, k):
         assert oracle.normwise_rel_err(Y[r], ref) <= TOL, (r, oracle.normwise_rel_err(Y[r], ref))
 
 
+@pytest.mark.parametrize("fmt", [(3, 64), (4, 128), (3, 32)], ids=lambda f: f"b{f[0]}g{f[1]}")
+@pytest.mark.parametrize("m,n", [(16, 300), (64, 300), (200, 4096), (512, 4096)], ids=lambda v: str(v))
+def test_gemm_a8_long_rows(gpu, fmt, m, n):
+    """Rows of more than 64 chunks (k = 11008), where the k split runs over 8 waves, at every
+    tile shape by m; sampled rows against the oracle's per-token A8 GEMV."""
+    qx = gpu
+    bits, g = fmt
+    k = 11008
+    print(f"a8 gemm long rows {fmt} m={m} n={n}", flush=True)
+    q = random_quant(n, k, bits, g, 0, seed=m + n + g)
+    X = _x_rows(m, k, seed=m + g)
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = qx.PackedWeight.from_quant(q).gemm_a8(Xq, sx).cpu().numpy()
+    for r in sorted(set(range(0, m, max(1, m // 6))) | {1, m - 1}):
+        ref = a8.gemv_a8(q.codes, g, q.scales, q.zeros, X[r])
+        if not np.any(ref):  # the all-zero token
+            assert not np.any(Y[r].astype(np.float32)), r
+            continue
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
+
+
 @pytest.mark.parametrize("bits,g", [(3, 128), (4, 32)])
 def test_gemm_a8_integer_results_are_exact(gpu, bits, g):
     """Scales 1, activations integers with one entry 127 per row (so inv = 1 and s_x = 1
