@@ -24,8 +24,9 @@
 // exact integers and one packed multiply (the same arithmetic as qx_dequant);
 // codebook weights are table entries fetched with v_perm_b32.
 //
-// Tiling. A block has four waves: KS of them split the chunks of a row
-// (round r gives wave ks chunk r*KS + ks) and 4/KS take different weight rows.
+// Tiling. A block has W waves (4, or 8 / 16 for rows of more than 64 chunks): KS of
+// them split the chunks of a row (round r gives wave ks chunk r*KS + ks) and W/KS
+// take different weight rows.
 // A wave owns 16*NT weight rows and 16*MT activation rows. Codes reach the
 // waves through LDS: the codes and group tables of the block's rows for the next
 // super-round (S rounds, S*KS chunks) are loaded in contiguous runs while the
@@ -39,7 +40,6 @@
 
 namespace qx {
 
-constexpr int kGemmThreads = 256;
 constexpr int kXRowBytes = 272;  // one activation row of one chunk (fragment order) + 16 B pad
 
 // Codes and group tables of one (weight row, chunk) as one lane needs them.

@@ -9,8 +9,9 @@
 // the A operand xq, and each k-step of 32 codes lies in one group (g >= 32), so a
 // group's int32 tile is scaled by its s and added to an fp32 tile when it ends.
 //
-// Work split: a block owns 16*(4/KS) weight rows (the MFMA columns; 16 per group of
-// KS waves) and 16*MT activation rows (the MFMA rows), and walks k KS chunks at a
+// Work split: a block of W waves (4, or 8 for rows of more than 64 chunks) owns
+// 16*(W/KS) weight rows (the MFMA columns; 16 per group of KS waves) and 16*MT
+// activation rows (the MFMA rows), and walks k KS chunks at a
 // time, wave ks of a group taking chunk ks: the chunks' activation tiles, codes and
 // group words go to LDS, the next ones are loaded into registers meanwhile, and the
 // KS partial tiles are added through LDS at the end. Lane group g (lane / 16) of
