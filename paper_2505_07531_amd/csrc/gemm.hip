@@ -526,13 +526,13 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
   const int cfg = QX_GEMM_CFG > 0 ? QX_GEMM_CFG : m <= 16 ? 1 : m <= 64 ? 2 : 4;
   switch (cfg) {
     case 1: {
-      // rows of more than 64 chunks: the k split over 8 waves (codebook) or 16 (uniform,
-      // m <= 8), each walking fewer chunks; codebook-3 4096x11008 at m = 16 took 24.7 us
-      // with 4 waves and 19.5 with 8, uniform-3 at m = 8 18.2 and 16.1 with 16 (shorter
-      // rows were slower split wider)
+      // rows of more than 64 chunks: the k split over 8 waves (codebook, Q4X) or 16
+      // (uniform, m <= 8), each walking fewer chunks; 4096x11008 at m = 16 took 24.7 us
+      // (codebook-3) and 24.6 (Q4X) with 4 waves, 19.5 and 19.2 with 8, uniform-3 at
+      // m = 8 18.2 and 16.1 with 16 (shorter rows were slower split wider)
       const int C = d->k / 128;
       const int w = QX_GEMM_SMALL_W != 4 ? QX_GEMM_SMALL_W
-                    : C > 64 ? (KIND == QX_CODEBOOK ? 8 : kUni && m <= 8 ? 16 : 4) : 4;
+                    : C > 64 ? (!kUni ? 8 : m <= 8 ? 16 : 4) : 4;
       if constexpr (kUni) {
         if (w == 16) launch_gemm_cfg<BITS, KIND, G, 1, 1, 16, 1, 1, A8, 16>(d, p, m, X, sx, Y, s);
         else if (w == 8) launch_gemm_cfg<BITS, KIND, G, 1, 1, 8, 1, 1, A8, 8>(d, p, m, X, sx, Y, s);

@@ -124,7 +124,7 @@ def test_q4x_max_k(gpu):
 
 GEMM_CASES = [(1, 40, 1152), (2, 40, 1152), (3, 130, 4096), (4, 4096, 4096), (2, 11008, 4096),
               (4, 300, 11008), (16, 100, 384), (17, 37, 11008), (64, 300, 1024), (65, 64, 4096),
-              (512, 260, 2048)]
+              (512, 260, 2048), (9, 130, 11008)]
 
 
 @pytest.mark.parametrize("m,n,k", GEMM_CASES, ids=lambda v: str(v))
