@@ -199,19 +199,22 @@ def cpu_baseline_decode():
         blob = qx.qx_pack_layout(qx.desc(q.n, q.k, q.bits, q.group, q.kind), q.codes, q.scales,
                                  q.zeros, q.codebook)
         items.append((spec, blob, configs.c4_activation(0, t), count))
-    step_s, total = 0.0, 0.0
+    step_s, total, reps = 0.0, 0.0, 3
     for spec, blob, x, count in items:
-        t0 = time.perf_counter()
-        w16 = oracle.dequant_packed(blob, spec.n, spec.k, spec.bits, spec.group, spec.kind)
-        oracle.gemv(w16, x)
-        dt = time.perf_counter() - t0
-        total += dt
-        step_s += dt * count
+        times = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            w16 = oracle.dequant_packed(blob, spec.n, spec.k, spec.bits, spec.group, spec.kind)
+            oracle.gemv(w16, x)
+            times.append(time.perf_counter() - t0)
+        total += sum(times)
+        step_s += float(np.median(times)) * count
     packed = sum(s.packed_bytes for s, _ in configs.c4_plan(32))
     return {"value": round(packed / step_s / 1e9, 4), "unit": "GB/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"3 GEMVs (layer-0 q, gate, down: unpack + fp16 dequant + fp64 matvec) in "
-                      f"{total:.1f} s, weighted x128/x64/x32 to a full step = "
+            "sample": f"3 GEMVs (layer-0 q, gate, down: unpack + fp16 dequant + fp64 matvec), each "
+                      f"timed {reps} times ({total:.1f} s in all); the medians weighted x128/x64/x32 "
+                      f"to a full step = "
                       f"{step_s * 1e3:.0f} ms per decode step; numpy elementwise work is "
                       f"single-threaded, BLAS uses the listed threads"}
 
