@@ -273,14 +273,17 @@ int launch_multi_t(const qx_desc* d, const void* packed, int m, const uint16_t* 
 // m = 1 and m = 2 and, when k > n, up to m = 4 (the GEMM then has few row tiles,
 // each with a long k loop); at m = 3, 4 with k <= n the GEMM is as fast or faster.
 // 4-bit codebooks of 32-code groups (a 32-byte table per 32 codes) decode faster
-// into matrix-core fragments at every m; at m = 2 so do 4-bit 64-code groups when
+// into matrix-core fragments at every m, except one row of 32 or 64 chunks, where the
+// group-per-lane GEMV is faster (11008x4096: 14.2 against 19.7 us); at m = 2 so do
+// 4-bit 64-code groups when
 // k <= n. Q4X (whose 16-entry lookups make the GEMM decode-bound) runs GEMV-style
 // for every m <= 4.
 bool gemv_multi_applies(const qx_desc* d, int m) {
   if (d->kind == QX_Q4X) return m >= 1 && m <= QX_MULTI_MAX_M;
   if (m < 1 || m > QX_MULTI_MAX_M) return false;
   const bool cb4 = d->kind == QX_CODEBOOK && d->bits == 4;
-  if (cb4 && d->group == 32) return false;
+  if (cb4 && d->group == 32)  // one row of 32 or 64 chunks: the group-per-lane GEMV
+    return m == 1 && (d->k == 32 * 128 || d->k == 64 * 128);
   if (m == 1 || d->k > d->n) return true;
   return m == 2 && !(cb4 && d->group == 64);
 }

@@ -185,10 +185,13 @@ def test_gemm_small_batch_longest_k(gpu, m):
         assert oracle.normwise_rel_err(Y[r], oracle.gemv(w16, X[r])) <= TOL, r
 
 
-def test_gemm_one_row_is_the_gemv(gpu):
-    """m = 1 runs the batch-1 GEMV: the same bits as qx_gemv."""
+@pytest.mark.parametrize("fmt", [(4, 0, 128), (4, 1, 32)], ids=_fmt_id)
+def test_gemm_one_row_is_the_gemv(gpu, fmt):
+    """m = 1 runs the batch-1 GEMV: the same bits as qx_gemv (the 4-bit codebook of
+    32-code groups too, on rows of 32 chunks)."""
     qx = gpu
-    q = realistic_quant(300, 4096, 4, 128, 0, seed=4)
+    bits, kind, g = fmt
+    q = realistic_quant(300, 4096, bits, g, kind, seed=4)
     pw = _pack(qx, q)
     x = activations(4096, seed=2)
     a = pw.gemm(to_dev(x[None, :])).cpu().numpy()[0]
