@@ -27,21 +27,40 @@ __device__ __forceinline__ void load_x(const uint16_t* __restrict__ x, int c0, i
   }
 }
 
-// Sums over one 16-byte piece of x (8 natural-order values at chunk position
-// 8*pc) for the folded zero point of uniform groups: sum x and sum M x, M the
-// bias that the decoder adds to the code at each position (b = 4: 1024 at even,
-// 64 at odd positions; b = 3: 1024 for codes 0-47, 128 for 48-95, 16 above).
-// Products of fp16 values are exact in fp32.
+// Sums over one 16-byte piece of x (8 values at chunk position 8*pc) for the
+// folded zero point of uniform groups: sum x, and sum M x with M the bias that
+// the decoder adds to the code at each position (b = 4: 1024 in bits 0-3, 64 in
+// bits 4-7 of a half; b = 3: 1024 for codes 0-47, 128 for 48-95, 16 above).
+// sum M x is formed exactly as chunk_dot forms the piece's sum of (M + q) x: one
+// dot2 chain over the decoder-order pairs o.x .. o.w, from 0, with the pair
+// (M, M) that the decoder yields for q = 0. So for a group whose codes are all
+// zero the two sums are the same bits and the group contributes exactly 0
+// (e.g. an all-zero group, which the quantizer stores with s = 1).
 template <int BITS>
-__device__ __forceinline__ void piece_sums(const u32x4& v, int pc, float& sx, float& mx) {
+__device__ __forceinline__ void piece_sums(const u32x4& v, const u32x4& o, int pc, float& sx,
+                                           float& mx) {
   const uint32_t one = 0x3C003C00u;  // (1, 1)
-  sx = dot2(v.w, one, dot2(v.z, one, dot2(v.y, one, dot2(v.x, one, 0.f))));
   if (BITS == 4) {
-    const uint32_t m = 0x54006400u;  // (1024, 64)
-    mx = dot2(v.w, m, dot2(v.z, m, dot2(v.y, m, dot2(v.x, m, 0.f))));
+    sx = dot2(v.w, one, dot2(v.z, one, dot2(v.y, one, dot2_0(v.x, one))));
+    const uint32_t m1024 = in_vgpr(kMagic1024), m64 = in_vgpr(0x54005400u);
+    mx = dot2(m64, o.w, dot2(m1024, o.z, dot2(m64, o.y, dot2_0(m1024, o.x))));
   } else {
+    // one M for the whole piece, a power of two: the chain of (M, M) pairs is M times
+    // the chain of (1, 1) pairs bit for bit (sums of binary16 values are never fp32
+    // subnormal, and M x cannot overflow)
+    const uint32_t o1 = in_vgpr(one);
+    sx = dot2(o1, o.w, dot2(o1, o.z, dot2(o1, o.y, dot2_0(o1, o.x))));
     mx = (pc < 6 ? 1024.f : pc < 12 ? 128.f : 16.f) * sx;
   }
+}
+
+// Sum of the N per-piece partial sums of one group in the balanced pairwise order
+// of lane_group_sum (xor 1, xor 2, half-row mirror, row mirror; fp32 addition is
+// commutative), the order in which the staged sum M x of the group was added.
+template <int N>
+__device__ __forceinline__ float piece_tree(const float* a) {
+  if constexpr (N == 1) return a[0];
+  else return piece_tree<N / 2>(a) + piece_tree<N / 2>(a + N / 2);
 }
 
 // Sum of v over aligned groups of N consecutive lanes (N = 4, 8, 16), in every lane.
@@ -65,25 +84,23 @@ __device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs,
   for (int i = 0; i < XP; ++i) {
     const int p = threadIdx.x + i * stride;
     const u32x4 v = xr[i];
-    if (EXACT || p < ct * 16) {
-      u32x4 o;
-      if (BITS == 4) {  // [x0 x1][x2 x3][x4 x5][x6 x7] -> [x0 x4][x1 x5][x2 x6][x3 x7]
-        o.x = perm(v.z, v.x, 0x05040100u);
-        o.y = perm(v.z, v.x, 0x07060302u);
-        o.z = perm(v.w, v.y, 0x05040100u);
-        o.w = perm(v.w, v.y, 0x07060302u);
-      } else {  // per 4: [x0 x1][x2 x3] -> [x0 x2][x1 x3]
-        o.x = perm(v.y, v.x, 0x05040100u);
-        o.y = perm(v.y, v.x, 0x07060302u);
-        o.z = perm(v.w, v.z, 0x05040100u);
-        o.w = perm(v.w, v.z, 0x07060302u);
-      }
-      *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
+    u32x4 o;
+    if (BITS == 4) {  // [x0 x1][x2 x3][x4 x5][x6 x7] -> [x0 x4][x1 x5][x2 x6][x3 x7]
+      o.x = perm(v.z, v.x, 0x05040100u);
+      o.y = perm(v.z, v.x, 0x07060302u);
+      o.z = perm(v.w, v.y, 0x05040100u);
+      o.w = perm(v.w, v.y, 0x07060302u);
+    } else {  // per 4: [x0 x1][x2 x3] -> [x0 x2][x1 x3]
+      o.x = perm(v.y, v.x, 0x05040100u);
+      o.y = perm(v.y, v.x, 0x07060302u);
+      o.z = perm(v.w, v.z, 0x05040100u);
+      o.w = perm(v.w, v.z, 0x07060302u);
     }
+    if (EXACT || p < ct * 16) *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
     if constexpr (KIND == QX_UNIFORM) {
       constexpr int PPG = G / 8;  // pieces per group
       float sx, mx;
-      piece_sums<BITS>(v, p & 15, sx, mx);
+      piece_sums<BITS>(v, o, p & 15, sx, mx);
       sx = lane_group_sum<PPG>(sx);
       mx = lane_group_sum<PPG>(mx);
       if ((p & (PPG - 1)) == 0 && (EXACT || p < ct * 16)) gs[p / PPG] = make_float2(mx, sx);
@@ -151,7 +168,10 @@ __device__ __forceinline__ uint32_t spare_sel(const Item<BITS, KIND, G>& it) {
 }
 
 // Scale and zero point of a uniform group word: s * (acc - sum M x - z sum x),
-// with acc = sum (M + q) x over the group, is s * sum (q - z) x.
+// with acc = sum (M + q) x over the group, is s * sum (q - z) x. acc and sum M x
+// are rounded in the same order (piece_sums, piece_tree): the difference is
+// exactly 0 when every code of the group is 0, and otherwise carries the rounding
+// of sums of (M + q) x, which s scales with the group's levels.
 __device__ __forceinline__ float fold_group(uint32_t word, float acc, float2 gsum) {
   const float s = half_bits_to_float(word & 0xFFFFu), z = half_bits_to_float(word >> 16);
   return s * (acc - gsum.x - z * gsum.y);
@@ -192,21 +212,21 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     }
     return part;
   } else if constexpr (BITS == 4 && KIND == 0) {
+    // one dot2 chain per 8-code piece, the pieces of a group added in the order of the
+    // staged sum M x (piece_sums, piece_tree)
+    float a[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const u32x4 x = xv[j];
+      const uint32_t D = it.d[j], Ds = D >> 8;
+      float acc = dot2_0((D & k.m000f) | k.mag1024, x.x);  // (0, 4)
+      acc = dot2((D & k.m00f0) | k.mag64, x.y, acc);          // (1, 5)
+      acc = dot2((Ds & k.m000f) | k.mag1024, x.z, acc);       // (2, 6)
+      a[j] = dot2((Ds & k.m00f0) | k.mag64, x.w, acc);        // (3, 7)
+    }
     float part = 0.f;
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      float acc = 0.f;
-#pragma unroll
-      for (int j = g * G / 8; j < (g + 1) * G / 8; ++j) {
-        const u32x4 x = xv[j];
-        const uint32_t D = it.d[j], Ds = D >> 8;
-        acc = dot2((D & k.m000f) | k.mag1024, x.x, acc);   // (0, 4)
-        acc = dot2((D & k.m00f0) | k.mag64, x.y, acc);     // (1, 5)
-        acc = dot2((Ds & k.m000f) | k.mag1024, x.z, acc);  // (2, 6)
-        acc = dot2((Ds & k.m00f0) | k.mag64, x.w, acc);    // (3, 7)
-      }
-      part += fold_group(it.m[g], acc, gs[g]);
-    }
+    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], piece_tree<G / 8>(a + g * (G / 8)), gs[g]);
     return part;
   } else if constexpr (BITS == 4 && KIND == 1) {
     float acc = 0.f;
@@ -228,21 +248,22 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     }
     return acc;
   } else if constexpr (BITS == 3 && KIND == 0) {
-    float acc[NG];
-#pragma unroll
-    for (int g = 0; g < NG; ++g) acc[g] = 0.f;
-    // x dwords of code block t (codes 4t..4t+3): 2t = pair (0,2), 2t+1 = pair (1,3)
-    const uint32_t* xd = reinterpret_cast<const uint32_t*>(xb);
+    // one dot2 chain per 8-code piece (x dwords 4p..4p+3): 4-code block t (codes
+    // 4t..4t+3) feeds x dwords 2t (pair (0,2)) and 2t+1 (pair (1,3)), so piece p is
+    // blocks 2p, 2p+1; pieces 0-5 are the bits 0-2 fields, 6-11 the bits 3-5 fields,
+    // 12-15 the spare codes. The pieces of a group are added as in piece_tree.
+    float a[16];
 #pragma unroll
     for (int i = 0; i < 12; ++i) {
       const U3Pairs p = u3_fields(it.d[i], k);
-      const int ga = (4 * i) / G, gb = (48 + 4 * i) / G;
-      const u32x2 xa = *reinterpret_cast<const u32x2*>(xd + 2 * i);
-      const u32x2 xb2 = *reinterpret_cast<const u32x2*>(xd + 2 * (12 + i));
-      acc[ga] = dot2(p.a0, xa.x, acc[ga]);
-      acc[ga] = dot2(p.a1, xa.y, acc[ga]);
-      acc[gb] = dot2(p.b0, xb2.x, acc[gb]);
-      acc[gb] = dot2(p.b1, xb2.y, acc[gb]);
+      const int pa = i / 2, pb = 6 + i / 2;
+      const u32x4 xa4 = xv[pa], xb4 = xv[pb];  // 16-byte pieces (one LDS read each per two i)
+      const uint32_t xa0 = (i & 1) ? xa4.z : xa4.x, xa1 = (i & 1) ? xa4.w : xa4.y;
+      const uint32_t xb0 = (i & 1) ? xb4.z : xb4.x, xb1 = (i & 1) ? xb4.w : xb4.y;
+      a[pa] = (i & 1) ? dot2(p.a0, xa0, a[pa]) : dot2_0(p.a0, xa0);
+      a[pa] = dot2(p.a1, xa1, a[pa]);
+      a[pb] = (i & 1) ? dot2(p.b0, xb0, a[pb]) : dot2_0(p.b0, xb0);
+      a[pb] = dot2(p.b1, xb1, a[pb]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -257,14 +278,15 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
         case 6: spare_pairs<6>(it, k, s0, s1); break;
         default: spare_pairs<7>(it, k, s0, s1); break;
       }
-      const int gg = (96 + 4 * i) / G;
-      const u32x2 xs = *reinterpret_cast<const u32x2*>(xd + 2 * (24 + i));
-      acc[gg] = dot2(s0, xs.x, acc[gg]);
-      acc[gg] = dot2(s1, xs.y, acc[gg]);
+      const int ps = 12 + i / 2;
+      const u32x4 xs4 = xv[ps];
+      const uint32_t xs0 = (i & 1) ? xs4.z : xs4.x, xs1 = (i & 1) ? xs4.w : xs4.y;
+      a[ps] = (i & 1) ? dot2(s0, xs0, a[ps]) : dot2_0(s0, xs0);
+      a[ps] = dot2(s1, xs1, a[ps]);
     }
     float part = 0.f;
 #pragma unroll
-    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], acc[g], gs[g]);
+    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], piece_tree<G / 8>(a + g * (G / 8)), gs[g]);
     return part;
   } else {  // BITS == 3, codebook
     LutGroup<3> t[NG];

@@ -189,22 +189,33 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
     const Item<BITS, KIND, G>& cur = it;
     __syncthreads();
 
-    float acc[M][NG];
+    // Uniform codes: one dot2 chain per 8-code piece (x dwords 4p..4p+3; every format
+    // emits a piece's pairs in slot order 0-3), the pieces of a group added as in
+    // piece_tree, so that all-zero codes reproduce the staged sum M x bit for bit.
+    // Table formats: one chain per group.
+    constexpr int NACC = KIND == QX_UNIFORM ? 16 : NG;
+    float acc[M][NACC];
 #pragma unroll
     for (int v = 0; v < M; ++v)
 #pragma unroll
-      for (int g = 0; g < NG; ++g) acc[v][g] = 0.f;
+      for (int g = 0; g < NACC; ++g) acc[v][g] = 0.f;
     for_each_pair<BITS, KIND, G>(cur, kc, q4lut, [&](int g, uint32_t pair, int xdw) {
 #pragma unroll
-      for (int v = 0; v < M; ++v)
-        acc[v][g] = dot2(pair, reinterpret_cast<const uint32_t*>(xb + v * xbytes)[xdw], acc[v][g]);
+      for (int v = 0; v < M; ++v) {
+        const uint32_t xv = reinterpret_cast<const uint32_t*>(xb + v * xbytes)[xdw];
+        if constexpr (KIND == QX_UNIFORM)
+          acc[v][xdw >> 2] = (xdw & 3) ? dot2(pair, xv, acc[v][xdw >> 2]) : dot2_0(pair, xv);
+        else
+          acc[v][g] = dot2(pair, xv, acc[v][g]);
+      }
     });
     if (c < cs) {
 #pragma unroll
       for (int v = 0; v < M; ++v) {
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
-          if constexpr (KIND == QX_UNIFORM) tot[v] += fold_group(cur.m[g], acc[v][g], gs[v * S * NG + c * NG + g]);
+          if constexpr (KIND == QX_UNIFORM)
+            tot[v] += fold_group(cur.m[g], piece_tree<G / 8>(&acc[v][g * (G / 8)]), gs[v * S * NG + c * NG + g]);
           else if constexpr (KIND == QX_Q4X) tot[v] += half_bits_to_float((cur.m[0] >> (16 * g)) & 0xFFFFu) * acc[v][g];
           else tot[v] += acc[v][g];
         }

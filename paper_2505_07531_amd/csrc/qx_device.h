@@ -44,6 +44,14 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float acc) {
   return __builtin_amdgcn_fdot2(as_h2(a), as_h2(b), acc, false);
 }
 
+// a.x*b.x + a.y*b.y from 0: the three-address v_dot2_f32_f16 with an inline 0
+// (the compiler otherwise zeroes a register for the accumulating two-address form).
+__device__ __forceinline__ float dot2_0(uint32_t a, uint32_t b) {
+  float r;
+  asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t hadd2(uint32_t a, uint32_t b) {
   return as_u32(as_h2(a) + as_h2(b));
 }
