@@ -95,37 +95,6 @@ __device__ __forceinline__ void read_lane_codes(LaneCodes<BITS, KIND, G>& lc, co
   }
 }
 
-// Dequantization constants of the uniform groups of one (row, chunk): the scale
-// pair (s, s) and -(M + z) pairs for the bias magic numbers M of each field.
-template <int BITS, int G>
-struct GroupConsts {
-  uint32_t sp[128 / G], z1024[128 / G], zb[128 / G], z16[128 / G];  // zb: M = 128 (b=3), 64 (b=4)
-};
-template <int BITS, int G>
-__device__ __forceinline__ GroupConsts<BITS, G> group_consts(const uint32_t* m) {
-  GroupConsts<BITS, G> gc;
-#pragma unroll
-  for (int i = 0; i < 128 / G; ++i) {
-    const uint32_t w = m[i];
-    // z is an integer-valued fp16 in [0, 2^b - 1]; -(M + z) is exact in fp16 and its bits
-    // are those of -M plus z fraction steps
-    const uint32_t z = (uint32_t)(unsigned short)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
-    gc.sp[i] = perm(w, w, 0x01000100u);
-    gc.z1024[i] = (0xE400u + z) * 0x00010001u;
-    gc.zb[i] = BITS == 3 ? (0xD800u + 8u * z) * 0x00010001u : (0xD400u + 16u * z) * 0x00010001u;
-    gc.z16[i] = (0xCC00u + 64u * z) * 0x00010001u;
-  }
-  return gc;
-}
-
-__device__ __forceinline__ uint32_t deq(uint32_t mq, uint32_t zc, uint32_t sp) {
-  return hmul2(hadd2(mq, zc), sp);  // fp16(s * (q - z)), q - z exact
-}
-
-__device__ __forceinline__ h8_t frag(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
-  return __builtin_bit_cast(h8_t, u32x4{a, b, c, d});
-}
-
 // B fragment of k-step T for this lane (weights in register pair order).
 template <int BITS, int KIND, int G, int T>
 __device__ __forceinline__ h8_t decode_frag(const LaneCodes<BITS, KIND, G>& lc,

@@ -9,11 +9,12 @@
 //     of the lane is issued before any is consumed; x is permuted into the pair
 //     order of the decoders and staged once per workgroup in LDS, padded so
 //     that lanes on consecutive chunks hit different banks;
-//   * codes are decoded in registers (qx_device.h), one v_and_or_b32 per code
-//     pair, and multiplied with v_dot2_f32_f16 (exact fp16 products, fp32
-//     sums); uniform codes enter as M + q and the zero point is folded out
-//     once per group with sums over x formed while x is staged, so no
-//     instruction per pair subtracts it; groups are scaled once;
+//   * codes are decoded in registers (qx_device.h), one or two VALU instructions
+//     per code pair, and multiplied with v_dot2_f32_f16 (exact fp16 products, fp32
+//     sums); uniform codes enter as subnormal integers (the masked field
+//     alone) and the zero point is folded out once per group with the sum of
+//     x formed while x is staged, so no instruction per pair subtracts it;
+//     groups are scaled once;
 //   * partial sums are reduced per row in a fixed order with DPP (no atomics;
 //     results are deterministic).
 //
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(64 * WPB) void gemv_wave_kernel(const char* __restr
   constexpr int C = LPR, NT = 64 * WPB, RPW = 64 / LPR, RPB = WPB * RPW;
   constexpr int XP = (C * 16 + NT - 1) / NT;
   __shared__ __align__(16) char xs[C * kXBlock];
-  __shared__ float2 gs[KIND == QX_UNIFORM ? C * (128 / G) : 1];
+  __shared__ float gs[KIND == QX_UNIFORM ? C * (128 / G) : 1];
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const int k = C * 128;
   const size_t meta_off = (size_t)n * k * BITS / 8;
@@ -75,7 +76,7 @@ __global__ __launch_bounds__(64 * WPB) void gemv_cb3_half_kernel(const char* __r
                                                                  uint16_t* __restrict__ y, int n) {
   constexpr int C = 32, NT = 64 * WPB, XP = (C * 16 + NT - 1) / NT;
   __shared__ __align__(16) char xs[C * kXBlock];
-  float2* no_gs = nullptr;  // codebook groups need no sums over x
+  float* no_gs = nullptr;  // codebook groups need no sums over x
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c = lane & 31, h = lane >> 5;
   const int row = blockIdx.x * WPB + wave;
@@ -196,7 +197,7 @@ __global__ __launch_bounds__(1024) void gemv_row_kernel(const char* __restrict__
   const int rows = min(R, n - row0);
   char* xs = smem;                                             // C * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + C * kXBlock);  // R * C floats
-  float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(C, R * C));  // C * 128/G
+  float* gs = reinterpret_cast<float*>(smem + row_lds_gsum_offset(C, R * C));  // C * 128/G
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const DecodeConsts kc = decode_consts();
 
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void gemv_tile_kernel(const char* __restr
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
   char* xs = smem;                                              // CT * kXBlock bytes
   float* part = reinterpret_cast<float*>(smem + CT * kXBlock);  // R * CT floats
-  float2* gs = reinterpret_cast<float2*>(smem + row_lds_gsum_offset(CT, R * CT));  // CT * 128/G
+  float* gs = reinterpret_cast<float*>(smem + row_lds_gsum_offset(CT, R * CT));  // CT * 128/G
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const DecodeConsts kc = decode_consts();
   if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);  // before the first barrier
@@ -316,7 +317,7 @@ static void launch_gemv_tile(const qx_desc* d, const char* p, const uint16_t* x,
   gemv_tile_shape(d->n, d->k, &R, &items);
   const int C = d->k / 128;
   const int CT = C <= kMaxTileChunks ? C : kLongTileChunks;
-  const size_t lds = (size_t)row_lds_gsum_offset(CT, R * CT) + (size_t)CT * (128 / G) * sizeof(float2);
+  const size_t lds = (size_t)row_lds_gsum_offset(CT, R * CT) + (size_t)CT * (128 / G) * sizeof(float);
   const dim3 grid((d->n + R - 1) / R), block(kThreads);
   const int xp = (CT * 16 + kThreads - 1) / kThreads;  // x pieces per thread: 1..6
 #define QX_GEMV_LAUNCH(I, XP) \
@@ -371,7 +372,7 @@ static int launch_gemv_t(const qx_desc* d, const void* packed, const uint16_t* x
     int R, threads;
     gemv_row_shape(d->n, C, KIND == QX_CODEBOOK && BITS == 4 && G == 32, &R, &threads);
     const unsigned blocks = (unsigned)((d->n + R - 1) / R);
-    const size_t lds = (size_t)row_lds_gsum_offset(C, R * C) + (size_t)C * (128 / G) * sizeof(float2);
+    const size_t lds = (size_t)row_lds_gsum_offset(C, R * C) + (size_t)C * (128 / G) * sizeof(float);
     const int xp = (C * 16 + threads - 1) / threads;
 #define QX_ROW_LAUNCH(XP) \
   hipLaunchKernelGGL((gemv_row_kernel<BITS, KIND, G, XP>), dim3(blocks), dim3(threads), lds, s, p, x, y, d->n, d->k, R)

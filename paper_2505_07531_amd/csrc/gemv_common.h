@@ -27,40 +27,12 @@ __device__ __forceinline__ void load_x(const uint16_t* __restrict__ x, int c0, i
   }
 }
 
-// Sums over one 16-byte piece of x (8 values at chunk position 8*pc) for the
-// folded zero point of uniform groups: sum x, and sum M x with M the bias that
-// the decoder adds to the code at each position (b = 4: 1024 in bits 0-3, 64 in
-// bits 4-7 of a half; b = 3: 1024 for codes 0-47, 128 for 48-95, 16 above).
-// sum M x is formed exactly as chunk_dot forms the piece's sum of (M + q) x: one
-// dot2 chain over the decoder-order pairs o.x .. o.w, from 0, with the pair
-// (M, M) that the decoder yields for q = 0. So for a group whose codes are all
-// zero the two sums are the same bits and the group contributes exactly 0
-// (e.g. an all-zero group, which the quantizer stores with s = 1).
-template <int BITS>
-__device__ __forceinline__ void piece_sums(const u32x4& v, const u32x4& o, int pc, float& sx,
-                                           float& mx) {
-  const uint32_t one = 0x3C003C00u;  // (1, 1)
-  if (BITS == 4) {
-    sx = dot2(v.w, one, dot2(v.z, one, dot2(v.y, one, dot2_0(v.x, one))));
-    const uint32_t m1024 = in_vgpr(kMagic1024), m64 = in_vgpr(0x54005400u);
-    mx = dot2(m64, o.w, dot2(m1024, o.z, dot2(m64, o.y, dot2_0(m1024, o.x))));
-  } else {
-    // one M for the whole piece, a power of two: the chain of (M, M) pairs is M times
-    // the chain of (1, 1) pairs bit for bit (sums of binary16 values are never fp32
-    // subnormal, and M x cannot overflow)
-    const uint32_t o1 = in_vgpr(one);
-    sx = dot2(o1, o.w, dot2(o1, o.z, dot2(o1, o.y, dot2_0(o1, o.x))));
-    mx = (pc < 6 ? 1024.f : pc < 12 ? 128.f : 16.f) * sx;
-  }
-}
-
-// Sum of the N per-piece partial sums of one group in the balanced pairwise order
-// of lane_group_sum (xor 1, xor 2, half-row mirror, row mirror; fp32 addition is
-// commutative), the order in which the staged sum M x of the group was added.
-template <int N>
-__device__ __forceinline__ float piece_tree(const float* a) {
-  if constexpr (N == 1) return a[0];
-  else return piece_tree<N / 2>(a) + piece_tree<N / 2>(a + N / 2);
+// Sum of one 16-byte piece of x (8 values) for the folded zero point of uniform
+// groups (one dot2 chain with the pair (1, 1); products of binary16 values are
+// exact in fp32).
+__device__ __forceinline__ float piece_sum(const u32x4& v) {
+  const uint32_t one = in_vgpr(0x3C003C00u);  // (1, 1)
+  return dot2(v.w, one, dot2(v.z, one, dot2(v.y, one, dot2_0(v.x, one))));
 }
 
 // Sum of v over aligned groups of N consecutive lanes (N = 4, 8, 16), in every lane.
@@ -75,10 +47,10 @@ __device__ __forceinline__ float lane_group_sum(float v) {
 
 // Permute the loaded pieces into decoder pair order and store them in LDS
 // (piece p of the tile: chunk p / 16, values 8 (p % 16) ..). For uniform
-// groups, also store (sum M x, sum x) per group of the tile in gs; the pieces
-// of a group sit in consecutive lanes.
+// groups, also store sum x per group of the tile in gs; the pieces of a group
+// sit in consecutive lanes.
 template <int BITS, int KIND, int G, int XP, bool EXACT = false>  // EXACT: every piece is in range
-__device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs, float2* gs,
+__device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs, float* gs,
                                         int stride = kThreads) {
 #pragma unroll
   for (int i = 0; i < XP; ++i) {
@@ -99,11 +71,8 @@ __device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs,
     if (EXACT || p < ct * 16) *reinterpret_cast<u32x4*>(xs + (p >> 4) * kXBlock + (p & 15) * 16) = o;
     if constexpr (KIND == QX_UNIFORM) {
       constexpr int PPG = G / 8;  // pieces per group
-      float sx, mx;
-      piece_sums<BITS>(v, o, p & 15, sx, mx);
-      sx = lane_group_sum<PPG>(sx);
-      mx = lane_group_sum<PPG>(mx);
-      if ((p & (PPG - 1)) == 0 && (EXACT || p < ct * 16)) gs[p / PPG] = make_float2(mx, sx);
+      const float sx = lane_group_sum<PPG>(piece_sum(v));
+      if ((p & (PPG - 1)) == 0 && (EXACT || p < ct * 16)) gs[p / PPG] = sx;
     }
   }
 }
@@ -158,31 +127,45 @@ __device__ __forceinline__ void load_item(Item<BITS, KIND, G>& it, const char* _
 // Bit-2 source dword of spare codes of code dword I, and the two spare helpers
 // dispatched on the compile-time index.
 template <int I, int BITS, int KIND, int G>
-__device__ __forceinline__ void spare_pairs(const Item<BITS, KIND, G>& it, const DecodeConsts& k,
-                                            uint32_t& s0, uint32_t& s1) {
-  u3_spare<I>(it.d[I], it.d[8 + (I & 3)], k, s0, s1);
+__device__ __forceinline__ void spare_raw(const Item<BITS, KIND, G>& it, const DecodeConsts& k,
+                                          uint32_t& s0, uint32_t& s1) {
+  u3_spare_raw<I>(it.d[I], it.d[8 + (I & 3)], k, s0, s1);
 }
 template <int I, int BITS, int KIND, int G>
 __device__ __forceinline__ uint32_t spare_sel(const Item<BITS, KIND, G>& it) {
   return u3_sel_spare<I>(it.d[I], it.d[8 + (I & 3)]);
 }
 
-// Scale and zero point of a uniform group word: s * (acc - sum M x - z sum x),
-// with acc = sum (M + q) x over the group, is s * sum (q - z) x. acc and sum M x
-// are rounded in the same order (piece_sums, piece_tree): the difference is
-// exactly 0 when every code of the group is 0, and otherwise carries the rounding
-// of sums of (M + q) x, which s scales with the group's levels.
-__device__ __forceinline__ float fold_group(uint32_t word, float acc, float2 gsum) {
+// Uniform codes enter the products unbiased, as binary16 subnormals: a code q in
+// fraction bits [f, f + b) of a half reads as q * 2^(f - 24) (the GEMV masks its
+// field out of the packed dword and nothing else). Products with x and their fp32
+// sums are exact up to the rounding of the sums, there is no bias whose sum over x
+// has to cancel, and a group whose codes are all 0 sums to exactly 0. Field kinds
+// per half: b = 4: bits 0-3 and 4-7; b = 3: bits 0-2, 3-5, 6-8 (spare codes).
+template <int BITS>
+struct RawFields {
+  static constexpr int kN = BITS == 4 ? 2 : 3;
+};
+// sum q x of one group from its per-field-kind accumulators f[0..kN)
+template <int BITS>
+__device__ __forceinline__ float raw_group_sum(const float* f) {
+  if constexpr (BITS == 4) return fmaf(f[1], 0x1p20f, f[0] * 0x1p24f);
+  else return fmaf(f[2], 0x1p18f, fmaf(f[1], 0x1p21f, f[0] * 0x1p24f));
+}
+
+// Scale and zero point of a uniform group word: s * (sum q x - z sum x) =
+// s * sum (q - z) x over the group; the error of both sums scales with s.
+__device__ __forceinline__ float fold_group(uint32_t word, float qx, float sx) {
   const float s = half_bits_to_float(word & 0xFFFFu), z = half_bits_to_float(word >> 16);
-  return s * (acc - gsum.x - z * gsum.y);
+  return s * fmaf(-z, sx, qx);
 }
 
 // Partial dot product of one chunk with its x block (LDS, pair order). Uniform
-// codes enter the products as M + q (no subtraction per pair); gs holds the
-// chunk's (sum M x, sum x) per group and fold_group takes the zero point out.
+// codes enter the products as subnormal integers (no subtraction per pair); gs
+// holds the chunk's sum x per group and fold_group takes the zero point out.
 template <int BITS, int KIND, int G>
 __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const char* xb,
-                                           const float2* gs, const DecodeConsts& k,
+                                           const float* gs, const DecodeConsts& k,
                                            const uint32_t* q4lut = nullptr) {
   constexpr int NG = 128 / G;
   const u32x4* xv = reinterpret_cast<const u32x4*>(xb);
@@ -212,21 +195,21 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     }
     return part;
   } else if constexpr (BITS == 4 && KIND == 0) {
-    // one dot2 chain per 8-code piece, the pieces of a group added in the order of the
-    // staged sum M x (piece_sums, piece_tree)
-    float a[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const u32x4 x = xv[j];
-      const uint32_t D = it.d[j], Ds = D >> 8;
-      float acc = dot2_0((D & k.m000f) | k.mag1024, x.x);  // (0, 4)
-      acc = dot2((D & k.m00f0) | k.mag64, x.y, acc);          // (1, 5)
-      acc = dot2((Ds & k.m000f) | k.mag1024, x.z, acc);       // (2, 6)
-      a[j] = dot2((Ds & k.m00f0) | k.mag64, x.w, acc);        // (3, 7)
-    }
     float part = 0.f;
 #pragma unroll
-    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], piece_tree<G / 8>(a + g * (G / 8)), gs[g]);
+    for (int g = 0; g < NG; ++g) {
+      float f[2] = {0.f, 0.f};  // bits 0-3, bits 4-7
+#pragma unroll
+      for (int j = g * G / 8; j < (g + 1) * G / 8; ++j) {
+        const u32x4 x = xv[j];
+        const uint32_t D = it.d[j], Ds = D >> 8;
+        f[0] = dot2(D & k.m000f, x.x, f[0]);   // (0, 4)
+        f[1] = dot2(D & k.m00f0, x.y, f[1]);   // (1, 5)
+        f[0] = dot2(Ds & k.m000f, x.z, f[0]);  // (2, 6)
+        f[1] = dot2(Ds & k.m00f0, x.w, f[1]);  // (3, 7)
+      }
+      part += fold_group(it.m[g], raw_group_sum<4>(f), gs[g]);
+    }
     return part;
   } else if constexpr (BITS == 4 && KIND == 1) {
     float acc = 0.f;
@@ -248,45 +231,46 @@ __device__ __forceinline__ float chunk_dot(const Item<BITS, KIND, G>& it, const 
     }
     return acc;
   } else if constexpr (BITS == 3 && KIND == 0) {
-    // one dot2 chain per 8-code piece (x dwords 4p..4p+3): 4-code block t (codes
-    // 4t..4t+3) feeds x dwords 2t (pair (0,2)) and 2t+1 (pair (1,3)), so piece p is
-    // blocks 2p, 2p+1; pieces 0-5 are the bits 0-2 fields, 6-11 the bits 3-5 fields,
-    // 12-15 the spare codes. The pieces of a group are added as in piece_tree.
-    float a[16];
+    // 4-code block t (codes 4t..4t+3) feeds x dwords 2t (pair (0,2)) and 2t+1 (pair
+    // (1,3)); blocks 0-11 are the bits 0-2 fields of code dwords 0-11, 12-23 their
+    // bits 3-5 fields, 24-31 the spare codes. One accumulator per (group, field kind).
+    float f[NG][3];
 #pragma unroll
-    for (int i = 0; i < 12; ++i) {
-      const U3Pairs p = u3_fields(it.d[i], k);
-      const int pa = i / 2, pb = 6 + i / 2;
-      const u32x4 xa4 = xv[pa], xb4 = xv[pb];  // 16-byte pieces (one LDS read each per two i)
-      const uint32_t xa0 = (i & 1) ? xa4.z : xa4.x, xa1 = (i & 1) ? xa4.w : xa4.y;
-      const uint32_t xb0 = (i & 1) ? xb4.z : xb4.x, xb1 = (i & 1) ? xb4.w : xb4.y;
-      a[pa] = (i & 1) ? dot2(p.a0, xa0, a[pa]) : dot2_0(p.a0, xa0);
-      a[pa] = dot2(p.a1, xa1, a[pa]);
-      a[pb] = (i & 1) ? dot2(p.b0, xb0, a[pb]) : dot2_0(p.b0, xb0);
-      a[pb] = dot2(p.b1, xb1, a[pb]);
+    for (int g = 0; g < NG; ++g) f[g][0] = f[g][1] = f[g][2] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 12; i += 2) {
+      const u32x4 xa = xv[i / 2], xb4 = xv[6 + i / 2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const U3Pairs p = u3_raw(it.d[i + h], k);
+        const int ga = (4 * (i + h)) / G, gb = (48 + 4 * (i + h)) / G;
+        f[ga][0] = dot2(p.a0, h ? xa.z : xa.x, f[ga][0]);
+        f[ga][0] = dot2(p.a1, h ? xa.w : xa.y, f[ga][0]);
+        f[gb][1] = dot2(p.b0, h ? xb4.z : xb4.x, f[gb][1]);
+        f[gb][1] = dot2(p.b1, h ? xb4.w : xb4.y, f[gb][1]);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       uint32_t s0, s1;
       switch (i) {  // the bit-2 position depends on the dword index at compile time
-        case 0: spare_pairs<0>(it, k, s0, s1); break;
-        case 1: spare_pairs<1>(it, k, s0, s1); break;
-        case 2: spare_pairs<2>(it, k, s0, s1); break;
-        case 3: spare_pairs<3>(it, k, s0, s1); break;
-        case 4: spare_pairs<4>(it, k, s0, s1); break;
-        case 5: spare_pairs<5>(it, k, s0, s1); break;
-        case 6: spare_pairs<6>(it, k, s0, s1); break;
-        default: spare_pairs<7>(it, k, s0, s1); break;
+        case 0: spare_raw<0>(it, k, s0, s1); break;
+        case 1: spare_raw<1>(it, k, s0, s1); break;
+        case 2: spare_raw<2>(it, k, s0, s1); break;
+        case 3: spare_raw<3>(it, k, s0, s1); break;
+        case 4: spare_raw<4>(it, k, s0, s1); break;
+        case 5: spare_raw<5>(it, k, s0, s1); break;
+        case 6: spare_raw<6>(it, k, s0, s1); break;
+        default: spare_raw<7>(it, k, s0, s1); break;
       }
-      const int ps = 12 + i / 2;
-      const u32x4 xs4 = xv[ps];
-      const uint32_t xs0 = (i & 1) ? xs4.z : xs4.x, xs1 = (i & 1) ? xs4.w : xs4.y;
-      a[ps] = (i & 1) ? dot2(s0, xs0, a[ps]) : dot2_0(s0, xs0);
-      a[ps] = dot2(s1, xs1, a[ps]);
+      const int gg = (96 + 4 * i) / G;
+      const u32x4 xs4 = xv[12 + i / 2];
+      f[gg][2] = dot2(s0, (i & 1) ? xs4.z : xs4.x, f[gg][2]);
+      f[gg][2] = dot2(s1, (i & 1) ? xs4.w : xs4.y, f[gg][2]);
     }
     float part = 0.f;
 #pragma unroll
-    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], piece_tree<G / 8>(a + g * (G / 8)), gs[g]);
+    for (int g = 0; g < NG; ++g) part += fold_group(it.m[g], raw_group_sum<3>(f[g]), gs[g]);
     return part;
   } else {  // BITS == 3, codebook
     LutGroup<3> t[NG];

@@ -15,9 +15,11 @@
 namespace qx {
 namespace {
 
-// Calls emit(group within the chunk, fp16 weight pair, x dword index within the
-// chunk's staged x block) for the 64 pairs of one item, in the decoders' pair order.
-// Uniform pairs are "M + q" (the zero point is folded per group by the caller).
+// Calls emit(accumulator slot, fp16 weight pair, x dword index within the chunk's
+// staged x block) for the 64 pairs of one item, in the decoders' pair order. Table
+// formats: slot = group within the chunk. Uniform codes: binary16 subnormals (the
+// masked field alone; the caller folds the zero point per group), slot = group *
+// RawFields<BITS>::kN + field kind, each kind with its own power-of-two unit.
 template <int BITS, int KIND, int G, typename F>
 __device__ __forceinline__ void for_each_pair(const Item<BITS, KIND, G>& it, const DecodeConsts& k,
                                               const uint32_t* q4lut, F&& emit) {
@@ -45,10 +47,10 @@ __device__ __forceinline__ void for_each_pair(const Item<BITS, KIND, G>& it, con
     for (int j = 0; j < 16; ++j) {
       const int g = (8 * j) / G;
       const uint32_t D = it.d[j], Ds = D >> 8;
-      emit(g, (D & k.m000f) | k.mag1024, 4 * j);       // (0, 4)
-      emit(g, (D & k.m00f0) | k.mag64, 4 * j + 1);     // (1, 5)
-      emit(g, (Ds & k.m000f) | k.mag1024, 4 * j + 2);  // (2, 6)
-      emit(g, (Ds & k.m00f0) | k.mag64, 4 * j + 3);    // (3, 7)
+      emit(2 * g, D & k.m000f, 4 * j);           // (0, 4)
+      emit(2 * g + 1, D & k.m00f0, 4 * j + 1);   // (1, 5)
+      emit(2 * g, Ds & k.m000f, 4 * j + 2);      // (2, 6)
+      emit(2 * g + 1, Ds & k.m00f0, 4 * j + 3);  // (3, 7)
     }
   } else if constexpr (BITS == 4 && KIND == QX_CODEBOOK) {
 #pragma unroll
@@ -69,29 +71,29 @@ __device__ __forceinline__ void for_each_pair(const Item<BITS, KIND, G>& it, con
   } else if constexpr (BITS == 3 && KIND == QX_UNIFORM) {
 #pragma unroll
     for (int i = 0; i < 12; ++i) {
-      const U3Pairs p = u3_fields(it.d[i], k);
+      const U3Pairs p = u3_raw(it.d[i], k);
       const int ga = (4 * i) / G, gb = (48 + 4 * i) / G;
-      emit(ga, p.a0, 2 * i);
-      emit(ga, p.a1, 2 * i + 1);
-      emit(gb, p.b0, 2 * (12 + i));
-      emit(gb, p.b1, 2 * (12 + i) + 1);
+      emit(3 * ga, p.a0, 2 * i);
+      emit(3 * ga, p.a1, 2 * i + 1);
+      emit(3 * gb + 1, p.b0, 2 * (12 + i));
+      emit(3 * gb + 1, p.b1, 2 * (12 + i) + 1);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       uint32_t s0, s1;
       switch (i) {
-        case 0: spare_pairs<0>(it, k, s0, s1); break;
-        case 1: spare_pairs<1>(it, k, s0, s1); break;
-        case 2: spare_pairs<2>(it, k, s0, s1); break;
-        case 3: spare_pairs<3>(it, k, s0, s1); break;
-        case 4: spare_pairs<4>(it, k, s0, s1); break;
-        case 5: spare_pairs<5>(it, k, s0, s1); break;
-        case 6: spare_pairs<6>(it, k, s0, s1); break;
-        default: spare_pairs<7>(it, k, s0, s1); break;
+        case 0: spare_raw<0>(it, k, s0, s1); break;
+        case 1: spare_raw<1>(it, k, s0, s1); break;
+        case 2: spare_raw<2>(it, k, s0, s1); break;
+        case 3: spare_raw<3>(it, k, s0, s1); break;
+        case 4: spare_raw<4>(it, k, s0, s1); break;
+        case 5: spare_raw<5>(it, k, s0, s1); break;
+        case 6: spare_raw<6>(it, k, s0, s1); break;
+        default: spare_raw<7>(it, k, s0, s1); break;
       }
       const int gg = (96 + 4 * i) / G;
-      emit(gg, s0, 2 * (24 + i));
-      emit(gg, s1, 2 * (24 + i) + 1);
+      emit(3 * gg + 2, s0, 2 * (24 + i));
+      emit(3 * gg + 2, s1, 2 * (24 + i) + 1);
     }
   } else {  // BITS == 3, codebook
     LutGroup<3> t[NG];
@@ -152,7 +154,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
   const int rows = min(R, n - row0);
   const int xbytes = S * kXBlock;
   float* part = reinterpret_cast<float*>(smem + M * xbytes);       // [M][R*S]
-  float2* gs = reinterpret_cast<float2*>(part + M * R * S);         // [M][S*NG] (uniform)
+  float* gs = part + M * R * S;                                    // [M][S*NG] (uniform)
   const DecodeConsts kc = decode_consts();
   const int t = threadIdx.x, r = t / S, c = t - r * S;
   const int row = row0 + min(r, rows - 1);
@@ -189,24 +191,18 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
     const Item<BITS, KIND, G>& cur = it;
     __syncthreads();
 
-    // Uniform codes: one dot2 chain per 8-code piece (x dwords 4p..4p+3; every format
-    // emits a piece's pairs in slot order 0-3), the pieces of a group added as in
-    // piece_tree, so that all-zero codes reproduce the staged sum M x bit for bit.
-    // Table formats: one chain per group.
-    constexpr int NACC = KIND == QX_UNIFORM ? 16 : NG;
-    float acc[M][NACC];
+    // one accumulator per slot and vector (for_each_pair)
+    constexpr int NF = KIND == QX_UNIFORM ? RawFields<BITS>::kN : 1;
+    float acc[M][NG * NF];
 #pragma unroll
     for (int v = 0; v < M; ++v)
 #pragma unroll
-      for (int g = 0; g < NACC; ++g) acc[v][g] = 0.f;
-    for_each_pair<BITS, KIND, G>(cur, kc, q4lut, [&](int g, uint32_t pair, int xdw) {
+      for (int g = 0; g < NG * NF; ++g) acc[v][g] = 0.f;
+    for_each_pair<BITS, KIND, G>(cur, kc, q4lut, [&](int slot, uint32_t pair, int xdw) {
 #pragma unroll
       for (int v = 0; v < M; ++v) {
         const uint32_t xv = reinterpret_cast<const uint32_t*>(xb + v * xbytes)[xdw];
-        if constexpr (KIND == QX_UNIFORM)
-          acc[v][xdw >> 2] = (xdw & 3) ? dot2(pair, xv, acc[v][xdw >> 2]) : dot2_0(pair, xv);
-        else
-          acc[v][g] = dot2(pair, xv, acc[v][g]);
+        acc[v][slot] = dot2(pair, xv, acc[v][slot]);
       }
     });
     if (c < cs) {
@@ -215,7 +211,7 @@ __global__ __launch_bounds__(512) void gemv_multi_kernel(const char* __restrict_
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
           if constexpr (KIND == QX_UNIFORM)
-            tot[v] += fold_group(cur.m[g], piece_tree<G / 8>(&acc[v][g * (G / 8)]), gs[v * S * NG + c * NG + g]);
+            tot[v] += fold_group(cur.m[g], raw_group_sum<BITS>(&acc[v][g * NF]), gs[v * S * NG + c * NG + g]);
           else if constexpr (KIND == QX_Q4X) tot[v] += half_bits_to_float((cur.m[0] >> (16 * g)) & 0xFFFFu) * acc[v][g];
           else tot[v] += acc[v][g];
         }
@@ -263,7 +259,7 @@ int launch_multi_m(const qx_desc* d, const char* p, int m, const uint16_t* X, ui
   multi_shape(C, &R, &S, &threads);
   if (threads < 16 * S || threads > 512) return QX_E_UNSUPPORTED;  // never with the shapes above
   const size_t lds = (size_t)M * S * kXBlock + (size_t)M * R * S * sizeof(float) +
-                     (KIND == QX_UNIFORM ? (size_t)M * S * (128 / G) * sizeof(float2) : 0);
+                     (KIND == QX_UNIFORM ? (size_t)M * S * (128 / G) * sizeof(float) : 0);
   const dim3 grid((unsigned)((d->n + R - 1) / R)), block(threads);
   hipLaunchKernelGGL((gemv_multi_kernel<BITS, KIND, G, M>), grid, block, lds, s, p, X, Y, d->n, d->k, m, R, S);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;

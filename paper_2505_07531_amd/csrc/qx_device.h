@@ -5,7 +5,9 @@
 // in the fraction bits of an fp16 whose exponent makes one fraction step
 // worth 1 reads as M + q (M = 1024 for bits 0-2/0-3, 128 for bits 3-5, 16 for
 // bits 6-8 of a half); subtracting the pair (M + z, M + z) with one packed
-// fp16 add leaves the exact integers q - z. Codebook entries are fetched with
+// fp16 add leaves the exact integers q - z. The GEMVs skip the bias: the code
+// field alone, masked out of its dword, is a binary16 subnormal q * 2^(f - 24)
+// (f its lowest fraction bit), which v_dot2 multiplies exactly. Codebook entries are fetched with
 // v_perm_b32, which picks bytes out of an 8-byte register table: the low and
 // the high bytes of the 2^b fp16 entries sit in separate tables, four codes
 // are looked up per instruction, and a final byte interleave rebuilds fp16
@@ -131,18 +133,28 @@ __device__ __forceinline__ U3Pairs u3_fields(uint32_t D, const DecodeConsts& k) 
   p.b1 = (Ds & k.m0038) | k.mag128;
   return p;
 }
+// The same fields as binary16 subnormals (no bias): a = (A0, A2), (A1, A3) read as
+// q * 2^-24, b = (B0, B2), (B1, B3) as q * 2^-21.
+__device__ __forceinline__ U3Pairs u3_raw(uint32_t D, const DecodeConsts& k) {
+  const uint32_t Ds = D >> 8;
+  U3Pairs p;
+  p.a0 = D & k.m0007;
+  p.a1 = Ds & k.m0007;
+  p.b0 = D & k.m0038;
+  p.b1 = Ds & k.m0038;
+  return p;
+}
 // Spare codes of code dword i (< 8): bits 0-1 in the spare fields of D, bit 2 in
 // H = dword 8 + (i & 3), bit 6 (i < 4) or bit 7 (i >= 4) of the matching byte.
-// Returns "16 + q" pairs for spare codes (0, 2) and (1, 3) of the dword.
+// Returns pairs for spare codes (0, 2) and (1, 3) of the dword in bits 6-8 of each
+// half, i.e. binary16 subnormals q * 2^-18.
 template <int I>
-__device__ __forceinline__ void u3_spare(uint32_t D, uint32_t H, const DecodeConsts& k,
-                                         uint32_t& s0, uint32_t& s1) {
+__device__ __forceinline__ void u3_spare_raw(uint32_t D, uint32_t H, const DecodeConsts& k,
+                                             uint32_t& s0, uint32_t& s1) {
   constexpr int kUp = (I < 4) ? 2 : 1;    // bit 6 or 7 of bytes 0/2 -> bit 8 of each half
   constexpr int kDown = (I < 4) ? 6 : 7;  // bit 6 or 7 of bytes 1/3 -> bit 8 of each half
-  const uint32_t t0 = ((H << kUp) & k.m0100) | k.mag16;
-  const uint32_t t1 = ((H >> kDown) & k.m0100) | k.mag16;
-  s0 = (D & k.m00c0) | t0;
-  s1 = ((D >> 8) & k.m00c0) | t1;
+  s0 = (D & k.m00c0) | ((H << kUp) & k.m0100);
+  s1 = ((D >> 8) & k.m00c0) | ((H >> kDown) & k.m0100);
 }
 // Byte selectors (4 codes, natural order) of the three fields of code dword D.
 __device__ __forceinline__ uint32_t u3_sel_a(uint32_t D) { return D & 0x07070707u; }
@@ -209,6 +221,37 @@ __device__ __forceinline__ void block_weights(uint32_t Q, const uint32_t* meta, 
     w01 = perm(hi, lo, 0x05010400u);
     w23 = perm(hi, lo, 0x07030602u);
   }
+}
+
+// Dequantization constants of the uniform groups of one (row, chunk): the scale
+// pair (s, s) and -(M + z) pairs for the bias magic numbers M of each field.
+template <int BITS, int G>
+struct GroupConsts {
+  uint32_t sp[128 / G], z1024[128 / G], zb[128 / G], z16[128 / G];  // zb: M = 128 (b=3), 64 (b=4)
+};
+template <int BITS, int G>
+__device__ __forceinline__ GroupConsts<BITS, G> group_consts(const uint32_t* m) {
+  GroupConsts<BITS, G> gc;
+#pragma unroll
+  for (int i = 0; i < 128 / G; ++i) {
+    const uint32_t w = m[i];
+    // z is an integer-valued fp16 in [0, 2^b - 1]; -(M + z) is exact in fp16 and its bits
+    // are those of -M plus z fraction steps
+    const uint32_t z = (uint32_t)(unsigned short)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+    gc.sp[i] = perm(w, w, 0x01000100u);
+    gc.z1024[i] = (0xE400u + z) * 0x00010001u;
+    gc.zb[i] = BITS == 3 ? (0xD800u + 8u * z) * 0x00010001u : (0xD400u + 16u * z) * 0x00010001u;
+    gc.z16[i] = (0xCC00u + 64u * z) * 0x00010001u;
+  }
+  return gc;
+}
+
+__device__ __forceinline__ uint32_t deq(uint32_t mq, uint32_t zc, uint32_t sp) {
+  return hmul2(hadd2(mq, zc), sp);  // fp16(s * (q - z)), q - z exact
+}
+
+__device__ __forceinline__ h8_t frag(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return __builtin_bit_cast(h8_t, u32x4{a, b, c, d});
 }
 
 // Cross-lane fp32 sums with DPP only (no LDS traffic). A DPP "row" is 16 lanes.
