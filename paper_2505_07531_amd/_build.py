@@ -15,7 +15,7 @@ PROBE_LIB = os.path.join(PKG, "libqxprobe.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["qx_api.cpp", "dequant.hip", "gemv.hip", "gemv_a8.hip", "gemv_lut_a8.hip", "gemv_multi.hip",
-           "gemm.hip", "gemm_a8.hip"]
+           "gemm.hip", "gemm_a8.hip", "gemm_skinny.hip"]
 PROBE_SOURCES = ["bw_probe.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc" if os.path.exists("/opt/rocm/bin/hipcc") else "hipcc")

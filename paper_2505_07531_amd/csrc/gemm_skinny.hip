@@ -1,0 +1,330 @@
+// Small-batch quantized GEMM on the matrix cores: Y[m][n] = sum_k X[m][k] W'[n][k]
+// for a few activation rows (decode of several sequences, short prefill chunks).
+//
+// With few activation rows the product is still bound by streaming the packed
+// weights (decoding is memory-bound, Section 2.4 of the paper), so this kernel
+// keeps the GEMV's access pattern and puts only the multiply on the matrix
+// cores:
+//
+//   * a lane owns one (weight row, 128-code chunk) item, read with b 16-byte
+//     loads from the slice planes, exactly as the GEMV reads it; no code byte
+//     goes through LDS;
+//   * the lane decodes its chunk into sixteen 8-weight pieces, each the B
+//     fragment of one v_mfma_f32_16x16x32_f16: lane l holds k-slice l / 16 of
+//     column l % 16, so the 16 lanes of a lane group are 16 weight rows on the
+//     same chunk, and the four lane groups are four chunks whose products the
+//     instruction adds;
+//   * uniform weights are dequantized exactly, fp16(s (q - z)), by one packed add
+//     of exact integers and one packed multiply (the arithmetic of qx_dequant),
+//     codebook weights are table entries fetched with v_perm_b32, Q4X entries
+//     times the group's scale;
+//   * the A fragment of a piece is the 8 activations of the piece's positions,
+//     loaded as 16 bytes per lane from X (L2-resident) and permuted into the
+//     decoder's pair order;
+//   * the W waves of a block share its 16*RF weight rows and split the chunks
+//     (wave w takes chunks 4(w + W j) .. + 3 for j < J); their 16x16 fp32 tiles are
+//     added in wave order through LDS, so results are deterministic.
+//
+// RF weight-row fragments share each A fragment; the m activation rows fill one
+// 16-row tile (rows past m repeat row m - 1 and are not stored). The A pieces come
+// from L2 per lane, a few pieces ahead of their products, so the kernel's time grows
+// with m; qx_gemm routes it where it measured faster (gemm_skinny_applies).
+#include "gemv_common.h"
+
+namespace qx {
+namespace {
+
+// Activation pieces in the decoders' pair order: b = 4 (0,4) (1,5) (2,6) (3,7);
+// b = 3 per four values (0,2) (1,3).
+template <int BITS>
+__device__ __forceinline__ h8_t x_frag(const u32x4 v) {
+  if constexpr (BITS == 4)
+    return frag(perm(v.z, v.x, 0x05040100u), perm(v.z, v.x, 0x07060302u), perm(v.w, v.y, 0x05040100u),
+                perm(v.w, v.y, 0x07060302u));
+  else
+    return frag(perm(v.y, v.x, 0x05040100u), perm(v.y, v.x, 0x07060302u), perm(v.w, v.z, 0x05040100u),
+                perm(v.w, v.z, 0x07060302u));
+}
+
+// Per-item decode tables: uniform scale / zero pairs, or the codebook (Q4X: the
+// selected sub-codebooks and the scale pairs) of the item's groups.
+template <int BITS, int KIND, int G>
+struct ItemTables {
+  static constexpr int NG = 128 / G;
+  GroupConsts<BITS, G> gc;  // uniform; Q4X uses sp
+  LutGroup<BITS> lut[KIND == QX_UNIFORM ? 1 : NG];
+};
+
+// valid = false (a chunk slot past the end of the row): tables whose every weight is
+// +-0, so that the slot adds nothing to the lane group's sum.
+template <int BITS, int KIND, int G>
+__device__ __forceinline__ ItemTables<BITS, KIND, G> item_tables(const Item<BITS, KIND, G>& it,
+                                                                 const uint32_t* q4lut, bool valid) {
+  ItemTables<BITS, KIND, G> t;
+  if constexpr (KIND == QX_UNIFORM) {
+    t.gc = group_consts<BITS, G>(it.m);
+#pragma unroll
+    for (int g = 0; g < 128 / G; ++g) t.gc.sp[g] = valid ? t.gc.sp[g] : 0u;  // s (q - z) -> +-0
+  } else if constexpr (KIND == QX_Q4X) {
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      t.gc.sp[g] = perm(it.m[0], it.m[0], g == 0 ? 0x01000100u : 0x03020302u);
+      const uint32_t* tp = q4lut + 8 * ((it.m[1] >> (2 * g)) & 3u);
+      const u32x4 tl = *reinterpret_cast<const u32x4*>(tp), th = *reinterpret_cast<const u32x4*>(tp + 4);
+      t.lut[g] = LutGroup<4>{{tl.x, tl.y, tl.z, tl.w}, {th.x, th.y, th.z, th.w}};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        t.lut[g].lo[i] = valid ? t.lut[g].lo[i] : 0u;
+        t.lut[g].hi[i] = valid ? t.lut[g].hi[i] : 0u;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int g = 0; g < 128 / G; ++g) {
+      t.lut[g] = lut_group<BITS>(&it.m[g << (BITS - 1)]);
+#pragma unroll
+      for (int i = 0; i < (1 << BITS) / 4; ++i) {
+        t.lut[g].lo[i] = valid ? t.lut[g].lo[i] : 0u;
+        t.lut[g].hi[i] = valid ? t.lut[g].hi[i] : 0u;
+      }
+    }
+  }
+  return t;
+}
+
+// B fragment of piece P (codes 8P .. 8P + 7 of the chunk) in the decoder's pair order.
+//   b = 4: code dword P;
+//   b = 3: P < 6: bits 0-2 fields of code dwords 2P, 2P + 1; 6 <= P < 12: bits 3-5
+//          fields of dwords 2(P - 6), 2(P - 6) + 1; P >= 12: spare codes of dwords
+//          2(P - 12), 2(P - 12) + 1 (bit 2 in dword 8 + (i & 3)).
+template <int BITS, int KIND, int G, int P>
+__device__ __forceinline__ h8_t piece_frag(const Item<BITS, KIND, G>& it, const ItemTables<BITS, KIND, G>& t,
+                                           const DecodeConsts& k) {
+  constexpr int gr = (8 * P) / G;  // the piece's group within the chunk
+  if constexpr (BITS == 4) {
+    const uint32_t D = it.d[P], Ds = D >> 8;
+    if constexpr (KIND == QX_UNIFORM) {
+      const GroupConsts<4, G>& gc = t.gc;
+      return frag(deq((D & k.m000f) | k.mag1024, gc.z1024[gr], gc.sp[gr]),   // (0, 4)
+                  deq((D & k.m00f0) | k.mag64, gc.zb[gr], gc.sp[gr]),       // (1, 5)
+                  deq((Ds & k.m000f) | k.mag1024, gc.z1024[gr], gc.sp[gr]),  // (2, 6)
+                  deq((Ds & k.m00f0) | k.mag64, gc.zb[gr], gc.sp[gr]));     // (3, 7)
+    } else {
+      uint32_t elo, ehi, olo, ohi;
+      lut4_bytes(t.lut[gr], D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
+      lut4_bytes(t.lut[gr], (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
+      const uint32_t p0 = perm(ehi, elo, 0x06020400u), p1 = perm(ohi, olo, 0x06020400u);
+      const uint32_t p2 = perm(ehi, elo, 0x07030501u), p3 = perm(ohi, olo, 0x07030501u);
+      if constexpr (KIND == QX_Q4X)  // fp16(s * CB[t][q]): one rounding, as qx_dequant
+        return frag(hmul2(p0, t.gc.sp[gr]), hmul2(p1, t.gc.sp[gr]), hmul2(p2, t.gc.sp[gr]),
+                    hmul2(p3, t.gc.sp[gr]));
+      return frag(p0, p1, p2, p3);
+    }
+  } else if constexpr (P < 12) {
+    constexpr bool kA = P < 6;
+    constexpr int i0 = kA ? 2 * P : 2 * (P - 6);
+    uint32_t w[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t D = it.d[i0 + h];
+      if constexpr (KIND == QX_UNIFORM) {
+        const U3Pairs p = u3_fields(D, k);
+        if constexpr (kA) {
+          w[2 * h] = deq(p.a0, t.gc.z1024[gr], t.gc.sp[gr]);
+          w[2 * h + 1] = deq(p.a1, t.gc.z1024[gr], t.gc.sp[gr]);
+        } else {
+          w[2 * h] = deq(p.b0, t.gc.zb[gr], t.gc.sp[gr]);
+          w[2 * h + 1] = deq(p.b1, t.gc.zb[gr], t.gc.sp[gr]);
+        }
+      } else {
+        lut3_pairs(t.lut[gr], kA ? u3_sel_a(D) : u3_sel_b(D), w[2 * h], w[2 * h + 1]);
+      }
+    }
+    return frag(w[0], w[1], w[2], w[3]);
+  } else {
+    uint32_t w[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      constexpr int kI0 = 2 * (P - 12);
+      const int i = kI0 + h;  // code dword of the spare codes; bit 2 in dword 8 + (i & 3)
+      const uint32_t D = it.d[kI0 + h], H = it.d[8 + ((kI0 + h) & 3)];
+      if constexpr (KIND == QX_UNIFORM) {
+        // bit 6 (dwords 0-3) or 7 (4-7) of bytes 0/2 and 1/3 of H -> bit 8 of each half
+        const uint32_t up = i < 4 ? 2u : 1u, dn = i < 4 ? 6u : 7u;
+        const uint32_t t0 = ((H << up) & k.m0100) | k.mag16;
+        const uint32_t t1 = ((H >> dn) & k.m0100) | k.mag16;
+        w[2 * h] = deq((D & k.m00c0) | t0, t.gc.z16[gr], t.gc.sp[gr]);
+        w[2 * h + 1] = deq(((D >> 8) & k.m00c0) | t1, t.gc.z16[gr], t.gc.sp[gr]);
+      } else {
+        const uint32_t ssh = i < 4 ? 4u : 5u;  // bit 6 or 7 of each byte -> bit 2
+        const uint32_t S = ((D >> 6) & 0x03030303u) | ((H >> ssh) & 0x04040404u);
+        lut3_pairs(t.lut[gr], S, w[2 * h], w[2 * h + 1]);
+      }
+    }
+    return frag(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Block: W = blockDim.x / 64 waves on weight rows n0 .. n0 + 16 RF - 1. Lane l of
+// wave w: column (weight row) n0 + 16 f + l % 16 of fragment f, chunk
+// 4 (w + W j) + l / 16 of item j, activation row m0 + 16 mt + l % 16 of tile mt.
+// LDS: W * RF * MT tiles of 16 x 16 fp32 for the wave-order reduction.
+template <int BITS, int KIND, int G, int RF, int MT, int J>
+__global__ __launch_bounds__(1024) void gemm_skinny_kernel(const char* __restrict__ packed,
+                                                           const uint16_t* __restrict__ X,
+                                                           uint16_t* __restrict__ Y, int n, int k, int m) {
+  extern __shared__ __align__(16) float red[];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
+  const int C = k >> 7, G_row = k / G, W = blockDim.x >> 6;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g = lane >> 4, li = lane & 15;
+  const int n0 = blockIdx.x * 16 * RF;
+  const DecodeConsts kc = decode_consts();
+
+  // codes and tables of every item of the lane, all loads issued first (rows and
+  // chunks clamped in bounds; chunks past C multiply zero activations)
+  Item<BITS, KIND, G> it[J][RF];
+  int cidx[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    cidx[j] = 4 * (wave + W * j) + g;
+#pragma unroll
+    for (int f = 0; f < RF; ++f)
+      load_item<BITS, KIND, G>(it[j][f], packed, meta_off, min(n0 + 16 * f + li, n - 1), min(cidx[j], C - 1), C,
+                               G_row);
+  }
+  if constexpr (KIND == QX_Q4X) {
+    stage_q4x_lut(packed, n, k, q4lut);
+    __syncthreads();
+  }
+  const uint16_t* xrow[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) xrow[mt] = X + (size_t)min(16 * mt + li, m - 1) * k;
+
+  f4_t acc[RF][MT];
+#pragma unroll
+  for (int f = 0; f < RF; ++f)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[f][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    if (4 * (wave + W * j) >= C) break;  // the wave's chunks of this item are all past C
+    const bool valid = cidx[j] < C;  // false only in the last item of a row
+    const u32x4* xp[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+      xp[mt] = reinterpret_cast<const u32x4*>(xrow[mt] + (size_t)min(cidx[j], C - 1) * 128);
+    ItemTables<BITS, KIND, G> tb[RF];
+#pragma unroll
+    for (int f = 0; f < RF; ++f) tb[f] = item_tables<BITS, KIND, G>(it[j][f], q4lut, valid);
+#define QX_SKINNY_PIECE(P)                                                                 \
+  {                                                                                        \
+    h8_t a[MT];                                                                            \
+    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                    \
+      a[mt] = x_frag<BITS>(xp[mt][P]);                                                     \
+    }                                                                                      \
+    _Pragma("unroll") for (int f = 0; f < RF; ++f) {                                       \
+      const h8_t b = piece_frag<BITS, KIND, G, P>(it[j][f], tb[f], kc);                    \
+      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) acc[f][mt] =                       \
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(a[mt], b, acc[f][mt], 0, 0, 0);           \
+    }                                                                                      \
+  }
+    QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
+    QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
+    QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
+    QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
+#undef QX_SKINNY_PIECE
+  }
+
+  // wave tiles -> LDS: red[((w * RF + f) * MT + mt) * 256 + 4 * lane + r] holds D[4 g + r][li]
+#pragma unroll
+  for (int f = 0; f < RF; ++f)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+      *reinterpret_cast<f4_t*>(red + ((wave * RF + f) * MT + mt) * 256 + 4 * lane) = acc[f][mt];
+  __syncthreads();
+  // output (row r of Y, column c) = tile (f = c / 16, mt = r / 16), element D[r % 16][c % 16]:
+  // lane 16 ((r % 16) / 4) + c % 16, register r % 4; waves added in order
+  constexpr int kOut = 256 * RF * MT;
+  for (int o = threadIdx.x; o < kOut; o += blockDim.x) {
+    const int c = o % (16 * RF), r = o / (16 * RF);
+    const int f = c >> 4, mt = r >> 4, rr = r & 15;
+    const int idx = (f * MT + mt) * 256 + 4 * (16 * (rr >> 2) + (c & 15)) + (rr & 3);
+    float s = 0.f;
+    for (int w = 0; w < W; ++w) s += red[w * RF * MT * 256 + idx];
+    if (r < m && n0 + c < n) Y[(size_t)r * n + n0 + c] = (uint16_t)float_to_half_bits(s);
+  }
+}
+
+template <int BITS, int KIND, int G, int RF, int MT, int J>
+int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
+  const int C = d->k / 128;
+  const int W = (C + 4 * J - 1) / (4 * J);
+  if (W > 16) return QX_E_UNSUPPORTED;
+  const size_t lds = (size_t)W * RF * MT * 256 * sizeof(float);
+  const unsigned blocks = (unsigned)((d->n + 16 * RF - 1) / (16 * RF));
+  hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, MT, J>), dim3(blocks), dim3(64 * W), lds, s, p, X, Y,
+                     d->n, d->k, m);
+  return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
+}
+
+#ifndef QX_SKINNY_RF
+#define QX_SKINNY_RF 0  // 0: by shape; 1, 2 force the weight-row fragments per wave
+#endif
+
+template <int BITS, int KIND, int G>
+int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
+  const char* p = static_cast<const char*>(packed);
+  const int C = d->k / 128;
+  const int J = (C + 63) / 64;  // items per lane: at most 16 waves of 4 chunks per item
+  const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : (d->n >= 8192 ? 2 : 1);
+  if (m > 16) return QX_E_UNSUPPORTED;
+  switch (J) {
+    case 1: return rf == 2 ? launch_cfg<BITS, KIND, G, 2, 1, 1>(d, p, m, X, Y, s)
+                           : launch_cfg<BITS, KIND, G, 1, 1, 1>(d, p, m, X, Y, s);
+    case 2: return rf == 2 ? launch_cfg<BITS, KIND, G, 2, 1, 2>(d, p, m, X, Y, s)
+                           : launch_cfg<BITS, KIND, G, 1, 1, 2>(d, p, m, X, Y, s);
+    case 3: return launch_cfg<BITS, KIND, G, 1, 1, 3>(d, p, m, X, Y, s);
+    case 4: return launch_cfg<BITS, KIND, G, 1, 1, 4>(d, p, m, X, Y, s);
+    default: return QX_E_UNSUPPORTED;
+  }
+}
+
+}  // namespace
+
+// Whether qx_gemm runs m rows on this kernel. Measured against the small-batch GEMV-style
+// kernel (m <= 4) and the matrix-core GEMM on 11008x4096, 4096x11008 and 4096x4096 in all
+// thirteen formats at m = 2-8 (us, 3-bit uniform g64: 11008x4096 m = 3 / 6: 11.9 / 14.3
+// against 16.3 / 16.0; 4096x11008 12.5 / 15.0 against 14.2 / 16.2; 4096x4096 5.5 / 6.0
+// against 8.8 / 8.7). The activation pieces come from L2 per lane, so its cost grows with
+// m and it loses beyond m = 4-8; 4-bit tables of 32 or 64 codes and, with two row
+// fragments per wave (n >= 8192), 3-bit tables of 32 or 64 codes and 4-bit ones of 128
+// hold too many registers; Q4X wins only on matrices of at most 4096 rows.
+bool gemm_skinny_applies(const qx_desc* d, int m) {
+  if (m < 2 || m > QX_SKINNY_MAX_M || d->k > 256 * 128) return false;
+  const bool cb = d->kind == QX_CODEBOOK, q4x = d->kind == QX_Q4X;
+  if (cb && d->bits == 4 && d->group <= 64) return false;
+  if (q4x) return d->n <= 4096 && m >= 3;
+  if (d->n <= 4096 && d->k <= 4096) return true;
+  if (m == 2) return false;
+  if (d->n >= 8192 && cb && (d->bits == 4 || d->group == 32)) return false;
+  const int mmax = d->bits == 4 || (d->n >= 8192 && cb && d->group == 64) ? 4 : 6;
+  return m <= mmax;
+}
+
+int launch_gemm_skinny(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y,
+                       hipStream_t s) {
+#define QX_SKINNY_CASE(B, K, G) \
+  if (d->bits == B && d->kind == K && d->group == G) return launch_t<B, K, G>(d, packed, m, X, Y, s);
+  QX_SKINNY_CASE(3, 0, 32) QX_SKINNY_CASE(3, 0, 64) QX_SKINNY_CASE(3, 0, 128)
+  QX_SKINNY_CASE(3, 1, 32) QX_SKINNY_CASE(3, 1, 64) QX_SKINNY_CASE(3, 1, 128)
+  QX_SKINNY_CASE(4, 0, 32) QX_SKINNY_CASE(4, 0, 64) QX_SKINNY_CASE(4, 0, 128)
+  QX_SKINNY_CASE(4, 1, 32) QX_SKINNY_CASE(4, 1, 64) QX_SKINNY_CASE(4, 1, 128)
+  QX_SKINNY_CASE(4, 2, 64)
+#undef QX_SKINNY_CASE
+  return QX_E_UNSUPPORTED;
+}
+
+}  // namespace qx

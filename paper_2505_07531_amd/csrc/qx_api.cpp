@@ -246,6 +246,9 @@ int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, 
   if (m == 0 || d->n == 0) return QX_OK;
   if (packed == nullptr || X == nullptr || Y == nullptr) return QX_E_ARG;
   if (!aligned16(packed) || !aligned16(X) || !aligned2(Y)) return QX_E_ARG;
+  if (m == 1 && qx::gemv_multi_applies(d, 1)) return qx::launch_gemv(d, packed, X, Y, stream);
+  // a few rows: the GEMV's chunk-per-lane loads with the products on the matrix cores
+  if (qx::gemm_skinny_applies(d, m)) return qx::launch_gemm_skinny(d, packed, m, X, Y, stream);
   if (qx::gemv_multi_applies(d, m))  // a few rows: decode every code once, GEMV-style
     return m == 1 ? qx::launch_gemv(d, packed, X, Y, stream)
                   : qx::launch_gemv_multi(d, packed, m, X, Y, stream);

@@ -1,0 +1,114 @@
+"""Parity of the small-batch matrix-core GEMM (qx_gemm at 2 <= m <= 8) with the oracle.
+
+That kernel keeps the GEMV's one-chunk-per-lane loads and multiplies on the
+matrix cores: a block's waves split each row's chunks 4 per wave and item (up
+to 4 items per lane, up to 16 waves) on 16 or 32 weight rows per block, and the
+m activation rows fill one 16-row tile. The cases below take each of those
+launch shapes at an m and shape that qx_gemm routes to it, with ragged rows,
+chunk slots past the end of a row and padded activation rows, in all thirteen
+formats (where a format is routed elsewhere the case checks that path). Every
+output row must be within the normwise bound of the oracle; a one-hot
+activation row must reproduce a column of W' exactly (the products are exact
+and the matrix cores add zeros), and repeated runs must be bitwise identical.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import q4x
+import qx_inputs as qi
+from qx_inputs import q4x as qq
+from helpers import TOL, activations, random_quant, to_dev
+
+pytestmark = pytest.mark.gpu
+
+FORMATS = [(b, kind, g) for b in (3, 4) for kind in (0, 1) for g in (32, 64, 128)] + [(4, 2, 64)]
+
+# (m, n, k): chunks per row C = k / 128 give 1-4 items per lane and 1-16 waves
+CASES = [
+    (2, 40, 384),      # C = 3: one wave, lane group 3 past the row
+    (5, 37, 1152),     # C = 9: 3 waves, the last with one valid lane group
+    (8, 130, 4096),    # C = 32: 8 waves
+    (3, 9, 8192),      # C = 64: 16 waves; n < 16
+    (4, 100, 11008),   # C = 86: 2 items, 11 waves
+    (4, 8200, 4096),   # two weight-row fragments per wave, last block ragged
+    (6, 60, 16384),    # C = 128: 2 items, 16 waves
+    (3, 20, 22016),    # C = 172: 3 items, 15 waves
+    (4, 33, 32768),    # C = 256: 4 items, 16 waves
+]
+
+
+def _fmt_id(f):
+    return f"b{f[0]}{'ucq'[f[1]]}g{f[2]}"
+
+
+def _quant(n, k, fmt, seed):
+    bits, kind, g = fmt
+    if kind == 2:
+        rng = np.random.default_rng(seed)
+        G = k // 64
+        s = np.float16(rng.uniform(0.25, 2.0, (n, G)) * rng.choice([-1.0, 1.0], (n, G), p=[0.1, 0.9]))
+        cb = np.sort(rng.standard_normal((4, 16)) * 0.05, axis=1).astype(np.float16).view(np.uint16)
+        return qi.QuantWeight(n, k, 4, 64, qq.Q4X, rng.integers(0, 16, (n, k), dtype=np.uint8),
+                              scales=s.view(np.uint16), codebook=cb,
+                              selectors=rng.integers(0, 4, (n, G), dtype=np.uint8))
+    return random_quant(n, k, bits, g, kind, seed=seed)
+
+
+def _w16(q):
+    if q.kind == 2:
+        return q4x.dequant(q.codes, q.scales, q.selectors, q.codebook)
+    return oracle.dequant(q.codes, q.group, q.kind, q.scales, q.zeros, q.codebook)
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"m{c[0]}_{c[1]}x{c[2]}")
+def test_skinny_matches_oracle(gpu, fmt, case):
+    qx = gpu
+    m, n, k = case
+    print(f"skinny {_fmt_id(fmt)} m={m} {n}x{k}", flush=True)
+    q = _quant(n, k, fmt, seed=n + k + m)
+    X = activations(k, seed=m + 7, m=m)
+    pw = qx.PackedWeight.from_quant(q)
+    Y = pw.gemm(to_dev(X)).cpu().numpy()
+    w16 = _w16(q)
+    rows = np.arange(n) if n <= 1024 else np.sort(np.random.default_rng(m).choice(n, 1024, replace=False))
+    rows = np.union1d(rows, [n - 1])  # the ragged last block
+    ref = oracle.gemm(X, w16[rows])
+    for r in range(m):
+        err = oracle.normwise_rel_err(Y[r][rows], ref[r])
+        assert err <= TOL, (r, err)
+    Y2 = pw.gemm(to_dev(X)).cpu().numpy()
+    assert np.array_equal(Y.view(np.uint16), Y2.view(np.uint16))  # deterministic
+
+
+@pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
+@pytest.mark.parametrize("m,n", [(4, 8200), (6, 4000)], ids=["m4_8200", "m6_4000"])
+def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n):
+    """Activation row r one-hot at position j_r: row r of Y equals column j_r of W' in
+    value (a sum that starts at +0 turns -0 weights into +0), on shapes with 2 items per
+    lane, a ragged last item, and 32-row (8200 rows) or 16-row blocks."""
+    qx = gpu
+    k = 11008
+    q = _quant(n, k, fmt, seed=m)
+    cols = np.random.default_rng(m + 1).choice(k, m, replace=False)
+    X = np.zeros((m, k), np.float16)
+    X[np.arange(m), cols] = 1.0
+    Y = qx.PackedWeight.from_quant(q).gemm(to_dev(X)).cpu().numpy()
+    ref = _w16(q)[:, cols].T
+    assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("m", [2, 6, 8])
+def test_skinny_rows_equal_gemv(gpu, m):
+    """Each row of the product against the batch-1 GEMV of the same row (two different
+    fp32 summation orders of the same products)."""
+    qx = gpu
+    q = random_quant(1000, 4096, 3, 64, 0, seed=m)
+    pw = qx.PackedWeight.from_quant(q)
+    X = activations(4096, seed=m + 1, m=m)
+    Y = pw.gemm(to_dev(X)).cpu().numpy()
+    for r in range(m):
+        y = pw.gemv(to_dev(X[r])).cpu().numpy()
+        assert oracle.normwise_rel_err(Y[r], y.astype(np.float64)) <= 2 * TOL, r
+
