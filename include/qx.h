@@ -205,9 +205,13 @@ int qx_quantize_a8(int32_t m, int32_t k, const uint16_t* X, int8_t* Xq, float* s
  *   uniform: sx[r] * sum_j s_j * sum_{k in group j} (q - z_j) * xq[r][k], the
  *     group sums exact (int8 matrix-core products, int32 accumulation), scaled
  *     in fp32;
- *   codebook and Q4X: sx[r] * sum_k W'[n][k] * xq[r][k] on the fp16 matrix
- *     cores (W' as qx_dequant gives it, the codes xq as exact fp16 integers,
- *     fp32 accumulation), scaled in fp32.
+ *   codebook: sx[r] * sum_k C_j[q] * xq[r][k] on the fp16 matrix cores (the
+ *     table entries and the codes xq as exact fp16 values, fp32 accumulation),
+ *     scaled in fp32;
+ *   Q4X: sx[r] * sum_j s_j * sum_{k in group j} CB[t_j][q] * xq[r][k], each
+ *     group's sum from the fp16 matrix cores scaled by s_j in fp32 (the exact
+ *     s * CB, as qx_gemv_a8; one row gives the same bits as qx_gemv_a8 on
+ *     the row the codes were quantized from when that row is one-hot).
  * m = 0 or n = 0 is a no-op; m must be <= 65536.
  */
 int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq, const float* sx,
@@ -218,10 +222,11 @@ int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq
  * Passage: as qx_gemv, batched over m rows.
  *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte
  *   alignment suffices for Y). fp16 products, fp32 accumulate, RNE to fp16:
- *   on the matrix cores with W' decoded exactly into their operands, or, for a
- *   few rows (m <= 4, by shape and format), GEMV-style with every code decoded
- *   once for all rows. m = 0 or n = 0 is a no-op; m must be <= 65536. All
- *   formats, Q4X included.
+ *   on the matrix cores with W' decoded exactly into their operands (for a few
+ *   rows, m <= 8 by shape and format, each lane decoding its own chunks as in
+ *   the GEMV), or, for m <= 4 where that measured faster, GEMV-style with every
+ *   code decoded once for all rows. m = 0 or n = 0 is a no-op; m must be
+ *   <= 65536. All formats, Q4X included. Deterministic.
  */
 int qx_gemm(const qx_desc* d, const void* packed, int32_t m, const uint16_t* X, uint16_t* Y,
             hipStream_t stream);

@@ -95,8 +95,9 @@ __device__ __forceinline__ void read_lane_codes(LaneCodes<BITS, KIND, G>& lc, co
   }
 }
 
-// B fragment of k-step T for this lane (weights in register pair order).
-template <int BITS, int KIND, int G, int T>
+// B fragment of k-step T for this lane (weights in register pair order). Q4X with
+// SCALE = false: the sub-codebook entries alone (the group's scale applied to the sum).
+template <int BITS, int KIND, int G, int T, bool SCALE = true>
 __device__ __forceinline__ h8_t decode_frag(const LaneCodes<BITS, KIND, G>& lc,
                                             const GroupConsts<BITS, G>& gc,
                                             const LutGroup<BITS> (&lut)[128 / G],
@@ -114,7 +115,7 @@ __device__ __forceinline__ h8_t decode_frag(const LaneCodes<BITS, KIND, G>& lc,
       uint32_t elo, ehi, olo, ohi;
       lut4_bytes(lut[gr], D & 0x0F0F0F0Fu, elo, ehi);         // codes 0 2 4 6
       lut4_bytes(lut[gr], (D >> 4) & 0x0F0F0F0Fu, olo, ohi);  // codes 1 3 5 7
-      if constexpr (KIND == QX_Q4X)  // fp16(s * CB[t][q]): one rounding, as qx_dequant
+      if constexpr (KIND == QX_Q4X && SCALE)  // fp16(s * CB[t][q]): one rounding, as qx_dequant
         return frag(hmul2(perm(ehi, elo, 0x06020400u), gc.sp[gr]), hmul2(perm(ohi, olo, 0x06020400u), gc.sp[gr]),
                     hmul2(perm(ehi, elo, 0x07030501u), gc.sp[gr]), hmul2(perm(ohi, olo, 0x07030501u), gc.sp[gr]));
       return frag(perm(ehi, elo, 0x06020400u), perm(ohi, olo, 0x06020400u),
@@ -338,6 +339,11 @@ __global__ __launch_bounds__(64 * W) void gemm_kernel(const char* __restrict__ p
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f4_t{0.f, 0.f, 0.f, 0.f};
+  // Q4X with 8-bit activations: k-steps 0-1 / 2-3 of a chunk are its groups 0 / 1; their
+  // sums of CB[t][q] * xq come from the matrix cores and are scaled by the group's s in
+  // fp32 (the exact s * CB of qx_gemv_a8, not W' rounded to binary16)
+  constexpr bool kQ4xGroupSums = A8 && KIND == QX_Q4X;
+  f4_t gsum[kQ4xGroupSums ? MT : 1][kQ4xGroupSums ? NT : 1];
 
   u32x4 cr[kCPieces], mr[kMPieces];
   if constexpr (KIND == QX_Q4X) stage_q4x_tables(packed + q4x_offsets(n, k).codebook, q4lut);
@@ -391,9 +397,20 @@ __global__ __launch_bounds__(64 * W) void gemm_kernel(const char* __restrict__ p
     _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const h8_t*>( \
         xb + (16 * mt + li) * kXRowBytes + 64 * (T) + 16 * g);                                \
     _Pragma("unroll") for (int nt = 0; nt < NT; ++nt) {                                       \
-      const h8_t b = decode_frag<BITS, KIND, G, T>(cur[nt], gc[nt], lut[nt], kc, up, dn, ssh); \
-      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) acc[mt][nt] =                         \
-          __builtin_amdgcn_mfma_f32_16x16x32_f16(a[mt], b, acc[mt][nt], 0, 0, 0);             \
+      const h8_t b = decode_frag<BITS, KIND, G, T, !kQ4xGroupSums>(cur[nt], gc[nt], lut[nt], kc, up, dn, ssh); \
+      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                     \
+        if constexpr (kQ4xGroupSums)                                                          \
+          gsum[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(                             \
+              a[mt], b, (T) % 2 == 0 ? f4_t{0.f, 0.f, 0.f, 0.f} : gsum[mt][nt], 0, 0, 0);     \
+        else                                                                                  \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[mt], b, acc[mt][nt], 0, 0, 0); \
+      }                                                                                       \
+    }                                                                                         \
+    if constexpr (kQ4xGroupSums && (T) % 2 == 1) { /* the group's scale on its sum */         \
+      _Pragma("unroll") for (int nt = 0; nt < NT; ++nt) {                                     \
+        const float sg = half_bits_to_float((cur[nt].m[0] >> (8 * (T) - 8)) & 0xFFFFu);       \
+        _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) acc[mt][nt] += sg * gsum[mt][nt];   \
+      }                                                                                       \
     }                                                                                         \
   }
         QX_GEMM_KSTEP(0)

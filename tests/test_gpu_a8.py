@@ -249,9 +249,9 @@ def test_codebook_gemv_a8_matches_oracle(gpu, fmt, shape):
 @pytest.mark.parametrize("shape", [(1, 130, 4096), (3, 300, 1152), (16, 257, 11008), (70, 1000, 2048),
                                    (256, 4096, 1024)], ids=lambda s: f"m{s[0]}_{s[1]}x{s[2]}")
 def test_table_gemm_a8_matches_oracle(gpu, fmt, shape):
-    """qx_gemm_a8 on codebook and Q4X weights: the int8 codes of qx_quantize_a8 times W' on the
-    fp16 matrix cores, scaled per row, against the per-row oracle of the same quantization (W'
-    rounded to binary16 for Q4X, as qx_dequant gives it: within the normwise bound)."""
+    """qx_gemm_a8 on codebook and Q4X weights: the int8 codes of qx_quantize_a8 times the table
+    entries on the fp16 matrix cores (Q4X: each group's sum scaled by its s in fp32), scaled
+    per row, against the per-row oracle of the same quantization."""
     import torch
     qx = gpu
     bits, kind, g = fmt
@@ -277,3 +277,38 @@ def test_table_gemm_a8_matches_oracle(gpu, fmt, shape):
     if m > 1:  # a row is the same product whatever else is in the batch
         y0 = pw.gemm_a8(Xq[:1].contiguous(), sx[:1].contiguous()).cpu().numpy()
         assert oracle.normwise_rel_err(y0[0], Y[0].astype(np.float64)) <= TOL
+
+
+@pytest.mark.parametrize("n,k", [(130, 4096), (300, 11008), (64, 1152)], ids=lambda v: str(v))
+def test_q4x_gemm_a8_is_the_gemv_a8_product(gpu, n, k):
+    """Q4X with 8-bit activations: qx_gemm_a8 multiplies the exact s * CB[t][q] like
+    qx_gemv_a8 (each group's sum of table entries times xq scaled by s in fp32), not W'
+    rounded to binary16. A one-hot row (x = a e_j, so xq = 127 e_j) gives one exact product
+    per output, which both calls scale in the same order: the same bits, for every group
+    and selector the probed columns touch; other rows stay within the bound of the oracle."""
+    import torch
+    from qx_inputs import q4x as qq
+    qx = gpu
+    rng = np.random.default_rng(n + k)
+    G = k // 64
+    s16 = np.float16(rng.uniform(0.3, 1.7, (n, G)) * rng.choice([-1.0, 1.0], (n, G))).view(np.uint16)
+    cb = np.sort(rng.standard_normal((4, 16)), axis=1).astype(np.float16).view(np.uint16)
+    q = qi.QuantWeight(n, k, 4, 64, qq.Q4X, rng.integers(0, 16, (n, k), dtype=np.uint8), scales=s16,
+                       codebook=cb, selectors=rng.integers(0, 4, (n, G), dtype=np.uint8))
+    pw = qx.PackedWeight.from_quant(q, device="cuda")
+    cols = rng.choice(k, 6, replace=False)
+    for j in cols:
+        x = np.zeros(k, np.float16)
+        x[j] = np.float16(rng.uniform(0.5, 3.0))
+        Xq, sx = qx.quantize_a8(to_dev(x[None, :]))
+        a = pw.gemm_a8(Xq, sx).cpu().numpy()[0]
+        b = pw.gemv_a8(to_dev(x)).cpu().numpy()
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16)), j
+    X = activations(k, seed=n, m=5)
+    Xq, sx = qx.quantize_a8(to_dev(X))
+    Y = pw.gemm_a8(Xq, sx).cpu().numpy()
+    for r in range(5):
+        ref = a8.gemv_a8_q4x(q.codes, q.scales, q.selectors, q.codebook, X[r])
+        assert oracle.normwise_rel_err(Y[r], ref) <= TOL, r
+        y = pw.gemv_a8(to_dev(X[r])).cpu().numpy()
+        assert oracle.normwise_rel_err(Y[r], y.astype(np.float64)) <= TOL, r
