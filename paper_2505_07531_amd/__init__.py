@@ -17,7 +17,9 @@ Functions keep the C names:
   qx_gemm_a8(desc, packed, m, Xq, sx, Y, stream=None)
   qx_status_str(status)
 Tensor arguments are torch CUDA tensors (HIP device memory); ``stream`` is a
-torch stream (default: the current stream).
+torch stream (default: the current stream). Before a device call the binding
+checks each tensor against the descriptor (device, dtype, contiguity, element
+count) and raises ValueError without launching anything when one does not fit.
 """
 from __future__ import annotations
 
@@ -152,12 +154,43 @@ def qx_pack_q4x(d: QxDesc, codes: np.ndarray, scales, selectors, codebook,
     return out[:size.value]
 
 
-def _dev_ptr(t):
+def _chk(t, name: str, dtype, numel: int):
+    """Check that `t` is a contiguous device tensor of `dtype` (None: any) holding at least
+    `numel` elements (the kernels read and write exactly the sizes the descriptor implies)."""
     if t is None:
-        return None
+        raise ValueError(f"{name}: a device tensor is required")
     if not t.is_cuda:
-        raise ValueError("device tensors required")
-    return ctypes.c_void_p(t.data_ptr())
+        raise ValueError(f"{name}: device tensors required")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {numel} needed")
+
+
+def _ptrs(*tensors):
+    """Device pointers, taken only once every argument has been checked."""
+    return [None if t is None else ctypes.c_void_p(t.data_ptr()) for t in tensors]
+
+
+def qx_blob_size(d: QxDesc) -> int:
+    """Bytes of the packed blob of `d` (any kind)."""
+    size = ctypes.c_size_t(0)
+    L = load()
+    fn = L.qx_pack_q4x if d.kind == QX_Q4X else L.qx_pack_layout
+    _check(fn(ctypes.byref(d), None, None, None, None, None, 0, ctypes.byref(size)), "packed size")
+    return size.value
+
+
+def _chk_packed(d: QxDesc, packed):
+    import torch
+    _chk(packed, "packed", torch.uint8, qx_blob_size(d))
+
+
+def _rows(X, m: int, k: int, name: str):
+    if X is not None and X.dim() == 2 and (X.shape[0] < m or X.shape[1] != k):
+        raise ValueError(f"{name}: shape {tuple(X.shape)}, expected ({m}, {k})")
 
 
 def _stream(stream):
@@ -167,33 +200,59 @@ def _stream(stream):
 
 
 def qx_dequant(d: QxDesc, packed, out_kind: int, out, stream=None) -> None:
-    _check(load().qx_dequant(ctypes.byref(d), _dev_ptr(packed), out_kind, _dev_ptr(out),
-                             _stream(stream)), "qx_dequant")
+    import torch
+    _chk_packed(d, packed)
+    _chk(out, "out", torch.float16 if out_kind == QX_OUT_F16 else torch.uint8, d.n * d.k)
+    _check(load().qx_dequant(ctypes.byref(d), *_ptrs(packed), out_kind, *_ptrs(out), _stream(stream)),
+           "qx_dequant")
 
 
 def qx_gemv(d: QxDesc, packed, x, y, stream=None) -> None:
-    _check(load().qx_gemv(ctypes.byref(d), _dev_ptr(packed), _dev_ptr(x), _dev_ptr(y),
-                          _stream(stream)), "qx_gemv")
+    import torch
+    _chk_packed(d, packed)
+    _chk(x, "x", torch.float16, d.k)
+    _chk(y, "y", torch.float16, d.n)
+    _check(load().qx_gemv(ctypes.byref(d), *_ptrs(packed, x, y), _stream(stream)), "qx_gemv")
 
 
 def qx_gemv_a8(d: QxDesc, packed, x, y, stream=None) -> None:
-    _check(load().qx_gemv_a8(ctypes.byref(d), _dev_ptr(packed), _dev_ptr(x), _dev_ptr(y),
-                             _stream(stream)), "qx_gemv_a8")
+    import torch
+    _chk_packed(d, packed)
+    _chk(x, "x", torch.float16, d.k)
+    _chk(y, "y", torch.float16, d.n)
+    _check(load().qx_gemv_a8(ctypes.byref(d), *_ptrs(packed, x, y), _stream(stream)), "qx_gemv_a8")
 
 
 def qx_gemm(d: QxDesc, packed, m: int, X, Y, stream=None) -> None:
-    _check(load().qx_gemm(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(X), _dev_ptr(Y),
-                          _stream(stream)), "qx_gemm")
+    import torch
+    m = int(m)
+    _chk_packed(d, packed)
+    _rows(X, m, d.k, "X")
+    _chk(X, "X", torch.float16, m * d.k)
+    _chk(Y, "Y", torch.float16, m * d.n)
+    p, x, y = _ptrs(packed, X, Y)
+    _check(load().qx_gemm(ctypes.byref(d), p, m, x, y, _stream(stream)), "qx_gemm")
 
 
 def qx_quantize_a8(m: int, k: int, X, Xq, sx, stream=None) -> None:
-    _check(load().qx_quantize_a8(int(m), int(k), _dev_ptr(X), _dev_ptr(Xq), _dev_ptr(sx),
-                                 _stream(stream)), "qx_quantize_a8")
+    import torch
+    m, k = int(m), int(k)
+    _chk(X, "X", torch.float16, m * k)
+    _chk(Xq, "Xq", torch.int8, m * k)
+    _chk(sx, "sx", torch.float32, m)
+    _check(load().qx_quantize_a8(m, k, *_ptrs(X, Xq, sx), _stream(stream)), "qx_quantize_a8")
 
 
 def qx_gemm_a8(d: QxDesc, packed, m: int, Xq, sx, Y, stream=None) -> None:
-    _check(load().qx_gemm_a8(ctypes.byref(d), _dev_ptr(packed), int(m), _dev_ptr(Xq), _dev_ptr(sx),
-                             _dev_ptr(Y), _stream(stream)), "qx_gemm_a8")
+    import torch
+    m = int(m)
+    _chk_packed(d, packed)
+    _rows(Xq, m, d.k, "Xq")
+    _chk(Xq, "Xq", torch.int8, m * d.k)
+    _chk(sx, "sx", torch.float32, m)
+    _chk(Y, "Y", torch.float16, m * d.n)
+    p, xq, s_, y = _ptrs(packed, Xq, sx, Y)
+    _check(load().qx_gemm_a8(ctypes.byref(d), p, m, xq, s_, y, _stream(stream)), "qx_gemm_a8")
 
 
 def quantize_a8(X, stream=None):

@@ -268,3 +268,53 @@ def test_a8_gemm_calls_reject_before_launch():
     assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 4, P(16), P(16), P(17), None) == qx.QX_E_ARG
     assert lib.qx_gemm_a8(ctypes.byref(d), P(16), 65537, P(16), P(16), P(16), None) == qx.QX_E_ARG
     assert lib.qx_gemm_a8(ctypes.byref(d), None, 0, None, None, None, None) == qx.QX_OK
+
+
+class _FakeTensor:
+    """Duck-typed stand-in for a device tensor: the binding's checks run, nothing launches."""
+
+    def __init__(self, dtype, numel, contiguous=True, cuda=True, shape=None):
+        self.dtype, self._n, self._c, self.is_cuda = dtype, numel, contiguous, cuda
+        self.shape = shape if shape is not None else (numel,)
+
+    def dim(self):
+        return len(self.shape)
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return 2
+
+    def is_contiguous(self):
+        return self._c
+
+    def data_ptr(self):
+        raise AssertionError("a pointer was taken: the call would have launched")
+
+
+def test_binding_checks_tensors_against_the_descriptor():
+    torch = pytest.importorskip("torch")
+    d = qx.desc(64, 256, 4, 128, 0)
+    blob = _FakeTensor(torch.uint8, qx.qx_packed_size(d))
+    x = _FakeTensor(torch.float16, 256)
+    y = _FakeTensor(torch.float16, 64)
+    bad = [
+        (_FakeTensor(torch.uint8, qx.qx_packed_size(d) - 1), x, y),    # short blob
+        (blob, _FakeTensor(torch.float32, 256), y),                    # x dtype
+        (blob, _FakeTensor(torch.float16, 255), y),                    # x too short
+        (blob, x, _FakeTensor(torch.float16, 63)),                     # y too short
+        (blob, _FakeTensor(torch.float16, 256, contiguous=False), y),  # strided x
+        (blob, _FakeTensor(torch.float16, 256, cuda=False), y),        # host x
+    ]
+    for b, xx, yy in bad:
+        with pytest.raises(ValueError):
+            qx.qx_gemv(d, b, xx, yy)
+    X = _FakeTensor(torch.float16, 4 * 256, shape=(4, 256))
+    with pytest.raises(ValueError):
+        qx.qx_gemm(d, blob, 4, _FakeTensor(torch.float16, 4 * 255, shape=(4, 255)), _FakeTensor(torch.float16, 256))
+    with pytest.raises(ValueError):
+        qx.qx_gemm(d, blob, 4, X, _FakeTensor(torch.float16, 4 * 64 - 1))
+    with pytest.raises(ValueError):
+        qx.qx_gemm_a8(d, blob, 4, _FakeTensor(torch.int8, 4 * 256, shape=(4, 256)), _FakeTensor(torch.float16, 4),
+                      _FakeTensor(torch.float16, 4 * 64))
