@@ -11,7 +11,9 @@ resident in HBM when the timed region starts.
 Printed (one JSON line): effective HBM GB/s on packed-weight bytes over the
 step (value), us per decode step, the roofline of the dominant kernel measured
 live (HIP events around a graph of its launches, on the stream they run on),
-and the CPU oracle timed on a bounded sample.
+and the CPU oracle timed on a bounded sample. Extra keys: gemv_configs (the
+single 4-bit and 3-bit GEMVs c1, c2, c3 with the plain read of the same bytes)
+and prefill_c5 (the MLP prefill GEMM at m = 16, 64, 512 against its roofline).
 
 Other workloads (each prints its own line): --workload c1|c2|c3 (single GEMV
 configs, rotated over enough copies to defeat the 256 MB last-level cache),
@@ -534,6 +536,57 @@ def bench_gemm(args, qx, a8=False, q4x=False):
     return lines
 
 
+def read_floor_us(nbytes: int, stream) -> float:
+    """us per launch of a plain coalesced read of `nbytes` (16 B per thread), cold: rotated
+    over copies >= 512 MB in a graph of back-to-back launches (the floor of a one-launch
+    GEMV of that many bytes)."""
+    import torch
+    from paper_2505_07531_amd import probe
+    dev = torch.device("cuda:0")
+    nbytes = -(-nbytes // 16) * 16
+    reps = max(2, -(-(512 << 20) // nbytes))
+    bufs = [torch.ones(nbytes, dtype=torch.uint8, device=dev) for _ in range(reps)]
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    def launch_all():
+        for b in bufs:
+            probe.qxp_read(b, sink)
+    us = time_graph(launch_all, stream, 5, 2) / reps * 1e3
+    del bufs
+    torch.cuda.empty_cache()
+    return us
+
+
+def gemv_config_summaries(args, qx):
+    """c1, c2, c3 (batch-1 GEMV, rotated copies, graph-timed) next to the plain read of the
+    same bytes: us, GB/s on packed bytes + x + y, % of 8 TB/s, % of the read's rate."""
+    import torch
+    out = {}
+    stream = torch.cuda.Stream()
+    for name in ("c1", "c2", "c3"):
+        line = bench_single_gemv(args, qx, name)
+        us = line["ms_per_step"] * 1e3
+        alg = line["config"]["packed_bytes"]
+        floor = read_floor_us(alg, stream)
+        out[name] = {"workload": line["config"]["workload"], "us": round(us, 3), "GBps": line["value"],
+                     "pct_of_hbm_peak": line["pct_of_hbm_peak"], "read_floor_us": round(floor, 3),
+                     "pct_of_read_floor": round(100 * floor / us, 1), "bytes": alg}
+        log(f"{name}: {us:.2f} us ({line['pct_of_hbm_peak']:.1f} % of 8 TB/s), read floor {floor:.2f} us")
+    return out
+
+
+def prefill_summary(args, qx):
+    """c5 (prefill GEMM on the MLP shapes, gate + up + down) at m = 16, 64, 512."""
+    out = {}
+    for line in bench_gemm(args, qx):
+        m = int(line["metric"].split("m=")[1].rstrip(")"))
+        rf = line["roofline"]
+        out[f"m{m}"] = {"us": round(line["ms_per_step"] * 1e3, 2), "TFLOPs": line["value"],
+                        "bound": rf["bound"], "achieved": rf["achieved"], "unit": rf["unit"],
+                        "frac_of_bound": rf["frac"]}
+        log(f"c5 m={m}: {line['ms_per_step'] * 1e3:.1f} us, {rf['frac'] * 100:.1f} % of the {rf['bound']} roof")
+    return out
+
+
 def bench_kernel_counters(args, qx):
     """Workload for counter passes: the dominant kernel (4-bit uniform GEMV on the fused
     22016x4096 gate|up matrix of layer 0) launched 20 times, then a 256 MiB device-to-device
@@ -604,6 +657,8 @@ def main():
                     choices=["decode7b", "batch", "c1", "c2", "c3", "c5", "c5a8", "q4x", "q4xgemm", "a8",
                              "tp8", "counters", "floor"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="decode7b only: skip the c1-c3 GEMV and c5 prefill keys")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path "
@@ -618,6 +673,9 @@ def main():
     log(f"device: {torch.cuda.get_device_name(0)}")
     if args.workload == "decode7b":
         out = bench_decode(args, qx)
+        if not args.no_configs:
+            out["gemv_configs"] = gemv_config_summaries(args, qx)
+            out["prefill_c5"] = prefill_summary(args, qx)
         if not args.no_cpu_baseline:
             t0 = time.time()
             out["cpu_baseline"] = cpu_baseline_decode()
