@@ -40,7 +40,12 @@ class MatrixSpec:
         return weights(self.dist, self.p, self.seed, self.stream, self.n, self.k, row0, rows)
 
     def quantized(self, row0: int = 0, rows: Optional[int] = None) -> QuantWeight:
-        q = quantize(self.weights(row0, rows), self.bits, self.group, self.kind)
+        """The quantized rows [row0, row0 + rows), from the disk cache when present."""
+        from . import cache
+        q = cache.load(self, row0, rows)
+        if q is None:
+            q = quantize(self.weights(row0, rows), self.bits, self.group, self.kind)
+            cache.store(self, row0, rows, q)
         q.meta["spec"] = self
         q.meta["row0"] = row0
         return q
