@@ -153,7 +153,10 @@ int qx_dequant(const qx_desc* d, const void* packed, int out_kind, void* out, hi
  *   packed  device blob; x fp16 [k]; y fp16 [n] (written, RNE from an fp32
  *           accumulator). y must not overlap x or packed.
  * Products of fp16 values are exact, sums are fp32 in a fixed order, so the
- * result is deterministic run to run. n = 0 is a no-op.
+ * result is deterministic run to run. Uniform groups are multiplied with their
+ * exact levels s*(q - z), the zero point taken out once per group, rather than
+ * with W' rounded to binary16: the two differ by that rounding (at most 2^-12
+ * of each weight). n = 0 is a no-op.
  */
 int qx_gemv(const qx_desc* d, const void* packed, const uint16_t* x, uint16_t* y,
             hipStream_t stream);

@@ -160,3 +160,24 @@ def test_gemv_a8_codebook_error_bound():
     _, s_x = a8.quantize_activation(x)
     bound = np.abs(w).sum(axis=1) * float(s_x) * (0.5 + 1e-5)
     assert np.all(np.abs(y - w @ x.astype(np.float64)) <= bound)
+
+
+def test_a8_reading_against_plain_rtn_on_the_workloads():
+    """The 8-bit activation codes are rint(x * fp32(127/amax)) with the product exact (the
+    kernels' arithmetic); plain round-to-nearest of x / (amax/127) in fp64 can differ only
+    where x*127/amax lies within an fp32 rounding of a half-integer. On c2 (outlier channels)
+    and the first 8 layers' decode-step activations the two readings differ in at most 1 in
+    1000 codes of a vector, each by 1 (none on c2)."""
+    from qx_inputs import configs
+    vectors = [configs.c2()[1]] + [configs.c4_activation(l, t) for l in range(8) for t in range(4)]
+    total = 0
+    for x in vectors:
+        xq, _ = a8.quantize_activation(x)
+        amax = np.max(np.abs(x.astype(np.float64)))
+        rtn = np.clip(np.rint(x.astype(np.float64) / (amax / 127.0)), -127, 127).astype(np.int64)
+        d = np.abs(xq.astype(np.int64) - rtn)
+        assert d.max() <= 1 and int(np.sum(d)) <= x.size // 1000
+        if x is vectors[0]:
+            assert not d.any()  # c2
+        total += int(np.sum(d))
+    print(f"codes differing from plain RTN: {total} of {sum(v.size for v in vectors)}")
