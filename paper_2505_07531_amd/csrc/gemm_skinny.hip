@@ -1,5 +1,5 @@
 // Small-batch quantized GEMM on the matrix cores: Y[m][n] = sum_k X[m][k] W'[n][k]
-// for a few activation rows (decode of several sequences, short prefill chunks).
+// for 2 <= m <= 16 activation rows (decode of several sequences, short prefill chunks).
 //
 // With few activation rows the product is still bound by streaming the packed
 // weights (decoding is memory-bound, Section 2.4 of the paper), so this kernel
@@ -18,17 +18,17 @@
 //     of exact integers and one packed multiply (the arithmetic of qx_dequant),
 //     codebook weights are table entries fetched with v_perm_b32, Q4X entries
 //     times the group's scale;
-//   * the A fragment of a piece is the 8 activations of the piece's positions,
-//     loaded as 16 bytes per lane from X (L2-resident) and permuted into the
-//     decoder's pair order;
+//   * the A fragment of a piece is the 8 activations of the piece's positions in
+//     the decoder's pair order; a wave stages the m activation rows of its four
+//     chunks in its own LDS rows with coalesced loads and reads the fragments
+//     from there (rows past m repeat row m - 1 and are not stored);
 //   * the W waves of a block share its 16*RF weight rows and split the chunks
 //     (wave w takes chunks 4(w + W j) .. + 3 for j < J); their 16x16 fp32 tiles are
 //     added in wave order through LDS, so results are deterministic.
 //
-// RF weight-row fragments share each A fragment; the m activation rows fill one
-// 16-row tile (rows past m repeat row m - 1 and are not stored). The A pieces come
-// from L2 per lane, a few pieces ahead of their products, so the kernel's time grows
-// with m; qx_gemm routes it where it measured faster (gemm_skinny_applies).
+// RF weight-row fragments share each A fragment: tall matrices take three per
+// wave, which puts one block on nearly every compute unit of an 11008-row matrix.
+// qx_gemm routes m rows here where it measured faster (gemm_skinny_applies).
 #include "gemv_common.h"
 
 namespace qx {
@@ -165,15 +165,34 @@ __device__ __forceinline__ h8_t piece_frag(const Item<BITS, KIND, G>& it, const 
   }
 }
 
+// One staged activation row of a wave's four chunks (1 KB) plus 16 bytes, so that
+// the 16 rows that one lane group reads start in different banks.
+constexpr int kXRow = 1024 + 16;
+
+#ifndef QX_SKINNY_PIN
+#define QX_SKINNY_PIN 1
+#endif
+
 // Block: W = blockDim.x / 64 waves on weight rows n0 .. n0 + 16 RF - 1. Lane l of
 // wave w: column (weight row) n0 + 16 f + l % 16 of fragment f, chunk
-// 4 (w + W j) + l / 16 of item j, activation row m0 + 16 mt + l % 16 of tile mt.
-// LDS: W * RF * MT tiles of 16 x 16 fp32 for the wave-order reduction.
-template <int BITS, int KIND, int G, int RF, int MT, int J>
-__global__ __launch_bounds__(1024) void gemm_skinny_kernel(const char* __restrict__ packed,
-                                                           const uint16_t* __restrict__ X,
-                                                           uint16_t* __restrict__ Y, int n, int k, int m) {
-  extern __shared__ __align__(16) float red[];
+// 4 (w + W j) + l / 16 of item j, activation row l % 16 (rows past m repeat row m - 1).
+//
+// Activations: the m rows of an item's four chunks are m contiguous 1 KB runs, so the
+// wave loads each run with one fully coalesced 16-byte-per-lane load (lane l: chunk
+// l / 16, piece l % 16), permutes it into the decoders' pair order and writes it to its
+// own LDS rows; each lane then reads its 16 A fragments (row l % 16, chunk l / 16)
+// from there. Reading the fragments straight from X would touch 64 cache lines per
+// load instead of 8.
+// Loads are issued in the order the products consume them: the first weight-row
+// fragment of item 0, item 0's activation rows, the other fragments and items; the
+// next item's activation rows are loaded while the current one is multiplied.
+// LDS: W * m rows of kXRow bytes, reused at the end for the W * RF tiles of 16 x 16
+// fp32 that are added in wave order.
+template <int BITS, int KIND, int G, int RF, int J, int LB>
+__global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict__ packed,
+                                                         const uint16_t* __restrict__ X,
+                                                         uint16_t* __restrict__ Y, int n, int k, int m) {
+  extern __shared__ __align__(16) char lds[];
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const int C = k >> 7, G_row = k / G, W = blockDim.x >> 6;
   const size_t meta_off = (size_t)n * k * BITS / 8;
@@ -181,137 +200,153 @@ __global__ __launch_bounds__(1024) void gemm_skinny_kernel(const char* __restric
   const int g = lane >> 4, li = lane & 15;
   const int n0 = blockIdx.x * 16 * RF;
   const DecodeConsts kc = decode_consts();
+  char* xs = lds + (size_t)wave * m * kXRow;  // this wave's activation rows
 
-  // codes and tables of every item of the lane, all loads issued first (rows and
-  // chunks clamped in bounds; chunks past C multiply zero activations)
   Item<BITS, KIND, G> it[J][RF];
-  int cidx[J];
+  auto load_frag = [&](int j, int f) {  // rows and chunks clamped in bounds
+    load_item<BITS, KIND, G>(it[j][f], packed, meta_off, min(n0 + 16 * f + li, n - 1),
+                             min(4 * (wave + W * j) + g, C - 1), C, G_row);
+  };
+  u32x4 xv[16];
+  auto load_x = [&](int j) {  // chunks past C clamped to the last (their weights are zero)
+    const uint16_t* src = X + (size_t)min(4 * (wave + W * j) + g, C - 1) * 128 + 8 * li;
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    cidx[j] = 4 * (wave + W * j) + g;
+    for (int r = 0; r < 16; ++r)
+      if (r < m) xv[r] = *reinterpret_cast<const u32x4*>(src + (size_t)r * k);
+  };
+  load_frag(0, 0);
+  load_x(0);
+  if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int f = 0; f < RF; ++f)
-      load_item<BITS, KIND, G>(it[j][f], packed, meta_off, min(n0 + 16 * f + li, n - 1), min(cidx[j], C - 1), C,
-                               G_row);
-  }
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int f = j == 0 ? 1 : 0; f < RF; ++f) load_frag(j, f);
+  if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
   if constexpr (KIND == QX_Q4X) {
     stage_q4x_lut(packed, n, k, q4lut);
     __syncthreads();
   }
-  const uint16_t* xrow[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) xrow[mt] = X + (size_t)min(16 * mt + li, m - 1) * k;
 
-  f4_t acc[RF][MT];
+  f4_t acc[RF];
 #pragma unroll
-  for (int f = 0; f < RF; ++f)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[f][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
+  for (int f = 0; f < RF; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     if (4 * (wave + W * j) >= C) break;  // the wave's chunks of this item are all past C
-    const bool valid = cidx[j] < C;  // false only in the last item of a row
-    const u32x4* xp[MT];
+    // stage the item's rows; the LDS instructions of one wave execute in order, so the
+    // reads below see these writes and the writes see the previous item's reads done
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      xp[mt] = reinterpret_cast<const u32x4*>(xrow[mt] + (size_t)min(cidx[j], C - 1) * 128);
-    ItemTables<BITS, KIND, G> tb[RF];
+    for (int r = 0; r < 16; ++r)
+      if (r < m) *reinterpret_cast<u32x4*>(xs + r * kXRow + 16 * lane) = __builtin_bit_cast(u32x4, x_frag<BITS>(xv[r]));
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    h8_t a[16];
+    {
+      const char* src = xs + min(li, m - 1) * kXRow + 256 * g;
 #pragma unroll
-    for (int f = 0; f < RF; ++f) tb[f] = item_tables<BITS, KIND, G>(it[j][f], q4lut, valid);
-#define QX_SKINNY_PIECE(P)                                                                 \
-  {                                                                                        \
-    h8_t a[MT];                                                                            \
-    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                    \
-      a[mt] = x_frag<BITS>(xp[mt][P]);                                                     \
-    }                                                                                      \
-    _Pragma("unroll") for (int f = 0; f < RF; ++f) {                                       \
-      const h8_t b = piece_frag<BITS, KIND, G, P>(it[j][f], tb[f], kc);                    \
-      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) acc[f][mt] =                       \
-          __builtin_amdgcn_mfma_f32_16x16x32_f16(a[mt], b, acc[f][mt], 0, 0, 0);           \
-    }                                                                                      \
-  }
-    QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
-    QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
-    QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
-    QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
+      for (int P = 0; P < 16; ++P) a[P] = *reinterpret_cast<const h8_t*>(src + 16 * P);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (j + 1 < J) load_x(j + 1);
+    const bool valid = 4 * (wave + W * j) + g < C;  // false only in the last item of a row
+#pragma unroll
+    for (int f = 0; f < RF; ++f) {
+      const ItemTables<BITS, KIND, G> tb = item_tables<BITS, KIND, G>(it[j][f], q4lut, valid);
+#define QX_SKINNY_PIECE(P) \
+  acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[P], piece_frag<BITS, KIND, G, P>(it[j][f], tb, kc), acc[f], 0, 0, 0);
+      QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
+      QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
+      QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
+      QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
 #undef QX_SKINNY_PIECE
+    }
   }
 
-  // wave tiles -> LDS: red[((w * RF + f) * MT + mt) * 256 + 4 * lane + r] holds D[4 g + r][li]
-#pragma unroll
-  for (int f = 0; f < RF; ++f)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      *reinterpret_cast<f4_t*>(red + ((wave * RF + f) * MT + mt) * 256 + 4 * lane) = acc[f][mt];
+  // wave tiles -> LDS (every wave is past its last read of its rows): red[(w * RF + f) * 256
+  // + 4 * lane + r] holds D[4 g + r][li]
   __syncthreads();
-  // output (row r of Y, column c) = tile (f = c / 16, mt = r / 16), element D[r % 16][c % 16]:
-  // lane 16 ((r % 16) / 4) + c % 16, register r % 4; waves added in order
-  constexpr int kOut = 256 * RF * MT;
-  for (int o = threadIdx.x; o < kOut; o += blockDim.x) {
+  float* red = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(red + (wave * RF + f) * 256 + 4 * lane) = acc[f];
+  __syncthreads();
+  // output (row r of Y, column c) = tile f = c / 16, element D[r][c % 16]:
+  // lane 16 (r / 4) + c % 16, register r % 4; waves added in order
+  for (int o = threadIdx.x; o < 256 * RF; o += blockDim.x) {
     const int c = o % (16 * RF), r = o / (16 * RF);
-    const int f = c >> 4, mt = r >> 4, rr = r & 15;
-    const int idx = (f * MT + mt) * 256 + 4 * (16 * (rr >> 2) + (c & 15)) + (rr & 3);
+    const int f = c >> 4;
+    const int idx = f * 256 + 4 * (16 * (r >> 2) + (c & 15)) + (r & 3);
     float s = 0.f;
-    for (int w = 0; w < W; ++w) s += red[w * RF * MT * 256 + idx];
+    for (int w = 0; w < W; ++w) s += red[w * RF * 256 + idx];
     if (r < m && n0 + c < n) Y[(size_t)r * n + n0 + c] = (uint16_t)float_to_half_bits(s);
   }
 }
 
-template <int BITS, int KIND, int G, int RF, int MT, int J>
+template <int BITS, int KIND, int G, int RF, int J, int LB>
 int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
   const int C = d->k / 128;
   const int W = (C + 4 * J - 1) / (4 * J);
-  if (W > 16) return QX_E_UNSUPPORTED;
-  const size_t lds = (size_t)W * RF * MT * 256 * sizeof(float);
+  if (W > LB / 64) return QX_E_UNSUPPORTED;
+  const size_t lds = std::max((size_t)W * m * kXRow, (size_t)W * RF * 256 * sizeof(float));
   const unsigned blocks = (unsigned)((d->n + 16 * RF - 1) / (16 * RF));
-  hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, MT, J>), dim3(blocks), dim3(64 * W), lds, s, p, X, Y,
+  hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB>), dim3(blocks), dim3(64 * W), lds, s, p, X, Y,
                      d->n, d->k, m);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 
 #ifndef QX_SKINNY_RF
-#define QX_SKINNY_RF 0  // 0: by shape; 1, 2 force the weight-row fragments per wave
+#define QX_SKINNY_RF 0  // 0: by shape; 1, 2, 3 force the weight-row fragments per wave
+#endif
+#ifndef QX_SKINNY_LB
+#define QX_SKINNY_LB 512  // threads per block at most (8 waves: up to 256 VGPRs per lane)
 #endif
 
 template <int BITS, int KIND, int G>
 int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
   const char* p = static_cast<const char*>(packed);
+  constexpr int LB = QX_SKINNY_LB, WMAX = LB / 64;
   const int C = d->k / 128;
-  const int J = (C + 63) / 64;  // items per lane: at most 16 waves of 4 chunks per item
-  const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : (d->n >= 8192 ? 2 : 1);
-  if (m > 16) return QX_E_UNSUPPORTED;
+  const int J = (C + 4 * WMAX - 1) / (4 * WMAX);  // items per lane
+  // tall matrices: three weight-row fragments per wave with one item per lane, two with
+  // two (the registers of three spill in some formats), one beyond
+  const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : (d->n >= 8192 ? (J == 1 ? 3 : J == 2 ? 2 : 1) : 1);
+  if (m < 1 || m > 16) return QX_E_UNSUPPORTED;
+#define QX_SKINNY_J(JJ)                                                                                   \
+  case JJ:                                                                                                \
+    return rf >= 3   ? launch_cfg<BITS, KIND, G, (JJ <= 2 ? 3 : 4 - JJ / 2), JJ, LB>(d, p, m, X, Y, s)   \
+           : rf == 2 ? launch_cfg<BITS, KIND, G, (JJ <= 3 ? 2 : 1), JJ, LB>(d, p, m, X, Y, s)             \
+                     : launch_cfg<BITS, KIND, G, 1, JJ, LB>(d, p, m, X, Y, s);
   switch (J) {
-    case 1: return rf == 2 ? launch_cfg<BITS, KIND, G, 2, 1, 1>(d, p, m, X, Y, s)
-                           : launch_cfg<BITS, KIND, G, 1, 1, 1>(d, p, m, X, Y, s);
-    case 2: return rf == 2 ? launch_cfg<BITS, KIND, G, 2, 1, 2>(d, p, m, X, Y, s)
-                           : launch_cfg<BITS, KIND, G, 1, 1, 2>(d, p, m, X, Y, s);
-    case 3: return launch_cfg<BITS, KIND, G, 1, 1, 3>(d, p, m, X, Y, s);
-    case 4: return launch_cfg<BITS, KIND, G, 1, 1, 4>(d, p, m, X, Y, s);
+    QX_SKINNY_J(1) QX_SKINNY_J(2) QX_SKINNY_J(3) QX_SKINNY_J(4)
     default: return QX_E_UNSUPPORTED;
   }
+#undef QX_SKINNY_J
 }
 
 }  // namespace
 
 // Whether qx_gemm runs m rows on this kernel. Measured against the small-batch GEMV-style
 // kernel (m <= 4) and the matrix-core GEMM on 11008x4096, 4096x11008 and 4096x4096 in all
-// thirteen formats at m = 2-8 (us, 3-bit uniform g64: 11008x4096 m = 3 / 6: 11.9 / 14.3
-// against 16.3 / 16.0; 4096x11008 12.5 / 15.0 against 14.2 / 16.2; 4096x4096 5.5 / 6.0
-// against 8.8 / 8.7). The activation pieces come from L2 per lane, so its cost grows with
-// m and it loses beyond m = 4-8; 4-bit tables of 32 or 64 codes and, with two row
-// fragments per wave (n >= 8192), 3-bit tables of 32 or 64 codes and 4-bit ones of 128
-// hold too many registers; Q4X wins only on matrices of at most 4096 rows.
+// thirteen formats at m = 2-16 (us, 3-bit uniform g64 at m = 2 / 8 / 16: 11008x4096 8.4 /
+// 9.0 / 9.9 against 9.2 / 15.7 / 15.8; 4096x11008 10.9 / 12.9 / 14.6 against 10.8 / 16.2 /
+// 18.1; 4096x4096 4.9 / 5.5 / 6.2 against 5.5 / 8.7 / 8.7). Rows of more than 32 chunks
+// take two or more items per lane, whose 4-bit tables of 32 or 64 codes (and, at more
+// than 4 items, any format) spill registers; Q4X, 4-bit codebooks of 128 codes and, at
+// m = 2, most formats run faster elsewhere on such rows.
 bool gemm_skinny_applies(const qx_desc* d, int m) {
-  if (m < 2 || m > QX_SKINNY_MAX_M || d->k > 256 * 128) return false;
+  const int C = d->k / 128, J = (C + 31) / 32;  // items per lane (8 waves of 4 chunks)
+#ifdef QX_SKINNY_FORCE
+  return m >= 2 && m <= 16 && J <= 4;
+#endif
+  if (m < 2 || m > QX_SKINNY_MAX_M || J > 4) return false;
   const bool cb = d->kind == QX_CODEBOOK, q4x = d->kind == QX_Q4X;
-  if (cb && d->bits == 4 && d->group <= 64) return false;
-  if (q4x) return d->n <= 4096 && m >= 3;
-  if (d->n <= 4096 && d->k <= 4096) return true;
-  if (m == 2) return false;
-  if (d->n >= 8192 && cb && (d->bits == 4 || d->group == 32)) return false;
-  const int mmax = d->bits == 4 || (d->n >= 8192 && cb && d->group == 64) ? 4 : 6;
-  return m <= mmax;
+  if (cb && d->bits == 4) return d->group >= 64 && J == 1;
+  if (q4x) return J == 1 && (m >= 3 || d->n <= 4096);
+  if (J >= 2 && m == 2) return cb && d->group >= 64;
+  return true;
 }
 
 int launch_gemm_skinny(const qx_desc* d, const void* packed, int m, const uint16_t* X, uint16_t* Y,

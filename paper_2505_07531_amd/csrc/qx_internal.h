@@ -62,9 +62,9 @@ int launch_gemv_multi(const qx_desc* d, const void* packed, int m, const uint16_
 
 // Products of 2 <= m <= QX_SKINNY_MAX_M rows on the matrix cores with the GEMV's
 // chunk-per-lane loads (gemm_skinny.hip; gemm_skinny_applies picks it per shape and
-// format); k up to 256 chunks.
+// format); k up to 128 chunks.
 #ifndef QX_SKINNY_MAX_M
-#define QX_SKINNY_MAX_M 8
+#define QX_SKINNY_MAX_M 16
 #endif
 bool gemm_skinny_applies(const qx_desc* d, int m);
 

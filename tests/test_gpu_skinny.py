@@ -1,15 +1,17 @@
-"""Parity of the small-batch matrix-core GEMM (qx_gemm at 2 <= m <= 8) with the oracle.
+"""Parity of the small-batch matrix-core GEMM (qx_gemm at 2 <= m <= 16) with the oracle.
 
 That kernel keeps the GEMV's one-chunk-per-lane loads and multiplies on the
 matrix cores: a block's waves split each row's chunks 4 per wave and item (up
-to 4 items per lane, up to 16 waves) on 16 or 32 weight rows per block, and the
-m activation rows fill one 16-row tile. The cases below take each of those
-launch shapes at an m and shape that qx_gemm routes to it, with ragged rows,
-chunk slots past the end of a row and padded activation rows, in all thirteen
-formats (where a format is routed elsewhere the case checks that path). Every
-output row must be within the normwise bound of the oracle; a one-hot
-activation row must reproduce a column of W' exactly (the products are exact
-and the matrix cores add zeros), and repeated runs must be bitwise identical.
+to 4 items per lane, up to 8 waves) on 16, 32 or 48 weight rows per block (one,
+two or three row fragments per wave), each wave stages the m activation rows of
+its chunks in LDS, and the m rows fill one 16-row tile. The cases below take
+each of those launch shapes at an m and shape that qx_gemm routes to it, with
+ragged rows, chunk slots past the end of a row, waves without a last item and
+padded activation rows, in all thirteen formats (where a format is routed
+elsewhere the case checks that path). Every output row must be within the
+normwise bound of the oracle; a one-hot activation row must reproduce a column
+of W' exactly (the products are exact and the matrix cores add zeros), and
+repeated runs must be bitwise identical.
 """
 import numpy as np
 import pytest
@@ -24,17 +26,20 @@ pytestmark = pytest.mark.gpu
 
 FORMATS = [(b, kind, g) for b in (3, 4) for kind in (0, 1) for g in (32, 64, 128)] + [(4, 2, 64)]
 
-# (m, n, k): chunks per row C = k / 128 give 1-4 items per lane and 1-16 waves
+# (m, n, k): chunks per row C = k / 128 give 1-4 items per lane (C <= 32, 64, 96, 128)
+# and 1-8 waves; 8192 rows or more take 3 (one item) or 2 (two items) row fragments
 CASES = [
-    (2, 40, 384),      # C = 3: one wave, lane group 3 past the row
-    (5, 37, 1152),     # C = 9: 3 waves, the last with one valid lane group
-    (8, 130, 4096),    # C = 32: 8 waves
-    (3, 9, 8192),      # C = 64: 16 waves; n < 16
-    (4, 100, 11008),   # C = 86: 2 items, 11 waves
-    (4, 8200, 4096),   # two weight-row fragments per wave, last block ragged
-    (6, 60, 16384),    # C = 128: 2 items, 16 waves
-    (3, 20, 22016),    # C = 172: 3 items, 15 waves
-    (4, 33, 32768),    # C = 256: 4 items, 16 waves
+    (2, 40, 384),       # C = 3: one wave, lane group 3 past the row
+    (5, 37, 1152),      # C = 9: 3 waves, the last with one valid lane group
+    (16, 130, 4096),    # C = 32: 8 waves, a full activation tile
+    (3, 9, 8192),       # C = 64: 2 items, 8 waves; n < 16
+    (12, 100, 11008),   # C = 86: 3 items, 8 waves, two waves without a third
+    (4, 8200, 4096),    # three row fragments per wave, last block ragged (40 of 48 rows)
+    (16, 8200, 4096),   # the same at a full activation tile
+    (7, 8193, 5120),    # C = 40: two row fragments per wave and 2 items; one row in the last block
+    (6, 60, 16384),     # C = 128: 4 items, 8 waves
+    (3, 20, 22016),     # C = 172: past the kernel's rows, routed elsewhere
+    (4, 33, 32768),     # C = 256: routed elsewhere
 ]
 
 
@@ -83,13 +88,13 @@ def test_skinny_matches_oracle(gpu, fmt, case):
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
-@pytest.mark.parametrize("m,n", [(4, 8200), (6, 4000)], ids=["m4_8200", "m6_4000"])
-def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n):
+@pytest.mark.parametrize("m,n,k", [(4, 8200, 11008), (6, 4000, 11008), (16, 8200, 4096)],
+                         ids=["m4_8200x11008", "m6_4000x11008", "m16_8200x4096"])
+def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n, k):
     """Activation row r one-hot at position j_r: row r of Y equals column j_r of W' in
-    value (a sum that starts at +0 turns -0 weights into +0), on shapes with 2 items per
-    lane, a ragged last item, and 32-row (8200 rows) or 16-row blocks."""
+    value (a sum that starts at +0 turns -0 weights into +0), on shapes with 3 items per
+    lane and a ragged last item (16-row blocks), and with 48-row blocks at m = 16."""
     qx = gpu
-    k = 11008
     q = _quant(n, k, fmt, seed=m)
     cols = np.random.default_rng(m + 1).choice(k, m, replace=False)
     X = np.zeros((m, k), np.float16)
@@ -99,7 +104,7 @@ def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n):
     assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))
 
 
-@pytest.mark.parametrize("m", [2, 6, 8])
+@pytest.mark.parametrize("m", [2, 6, 8, 13, 16])
 def test_skinny_rows_equal_gemv(gpu, m):
     """Each row of the product against the batch-1 GEMV of the same row (two different
     fp32 summation orders of the same products)."""
