@@ -183,9 +183,9 @@ constexpr int kXRow = 1024 + 16;
 // own LDS rows; each lane then reads its 16 A fragments (row l % 16, chunk l / 16)
 // from there. Reading the fragments straight from X would touch 64 cache lines per
 // load instead of 8.
-// Loads are issued in the order the products consume them: the first weight-row
-// fragment of item 0, item 0's activation rows, the other fragments and items; the
-// next item's activation rows are loaded while the current one is multiplied.
+// Loads are issued in the order the products consume them: item 0's activation rows,
+// the first weight-row fragment of item 0, the other fragments and items; the next
+// item's activation rows are loaded while the current one is multiplied.
 // LDS: W * m rows of kXRow bytes, reused at the end for the W * RF tiles of 16 x 16
 // fp32 that are added in wave order.
 template <int BITS, int KIND, int G, int RF, int J, int LB>
@@ -204,8 +204,8 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
 
   Item<BITS, KIND, G> it[J][RF];
   auto load_frag = [&](int j, int f) {  // rows and chunks clamped in bounds
-    load_item<BITS, KIND, G>(it[j][f], packed, meta_off, min(n0 + 16 * f + li, n - 1),
-                             min(4 * (wave + W * j) + g, C - 1), C, G_row);
+    load_item<BITS, KIND, G, J == 1>(it[j][f], packed, meta_off, min(n0 + 16 * f + li, n - 1),
+                                     min(4 * (wave + W * j) + g, C - 1), C, G_row);
   };
   u32x4 xv[16];
   auto load_x = [&](int j) {  // chunks past C clamped to the last (their weights are zero)
@@ -214,8 +214,9 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
     for (int r = 0; r < 16; ++r)
       if (r < m) xv[r] = *reinterpret_cast<const u32x4*>(src + (size_t)r * k);
   };
+  load_x(0);  // small and L2-resident: first, so that staging waits for it alone
+  if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
   load_frag(0, 0);
-  load_x(0);
   if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int j = 0; j < J; ++j)

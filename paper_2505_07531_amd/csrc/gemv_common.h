@@ -78,6 +78,12 @@ __device__ __forceinline__ void store_x(const u32x4 (&xr)[XP], int ct, char* xs,
 }
 
 // Raw bytes of one item: codes (4*BITS dwords) and its group tables.
+template <bool NT, typename T>
+__device__ __forceinline__ T ld_nt(const T* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
 template <int BITS, int KIND, int G>
 struct Item {
   static constexpr int kGroups = 128 / G;
@@ -87,21 +93,24 @@ struct Item {
   uint32_t m[kMetaDw];
 };
 
-template <int BITS, int KIND, int G>
+// Codes and tables of one (row, chunk) item. NT: non-temporal loads (streamed once);
+// the small-batch kernel reads each 128-byte line as two halves from two items and
+// keeps them cached when a lane has more than one item.
+template <int BITS, int KIND, int G, bool NT = true>
 __device__ __forceinline__ void load_item(Item<BITS, KIND, G>& it, const char* __restrict__ packed,
                                           size_t meta_off, int row, int c, int C, int G_row) {
   const u32x4* code = reinterpret_cast<const u32x4*>(packed) + ((size_t)row * BITS * C + c);
 #pragma unroll
   for (int s = 0; s < BITS; ++s) {
-    const u32x4 v = __builtin_nontemporal_load(code + (size_t)s * C);
+    const u32x4 v = ld_nt<NT>(code + (size_t)s * C);
     it.d[4 * s + 0] = v.x; it.d[4 * s + 1] = v.y; it.d[4 * s + 2] = v.z; it.d[4 * s + 3] = v.w;
   }
   if constexpr (KIND == QX_Q4X) {  // groups 2c and 2c + 1 of the row
     const size_t sel_off = meta_off + meta_off / 16;  // after n*G binary16 scales (n*k/32 bytes)
     const int W = (G_row + 15) / 16;
-    it.m[0] = __builtin_nontemporal_load(
+    it.m[0] = ld_nt<NT>(
         reinterpret_cast<const uint32_t*>(packed + meta_off + ((size_t)row * G_row + 2 * c) * 2));
-    const uint32_t sw = __builtin_nontemporal_load(
+    const uint32_t sw = ld_nt<NT>(
         reinterpret_cast<const uint32_t*>(packed + sel_off + ((size_t)row * W + c / 8) * 4));
     it.m[1] = (sw >> (4 * (c % 8))) & 0xFu;
     return;
@@ -113,14 +122,14 @@ __device__ __forceinline__ void load_item(Item<BITS, KIND, G>& it, const char* _
   if constexpr (kDw % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < kDw / 4; ++i) {
-      const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(mp) + i);
+      const u32x4 v = ld_nt<NT>(reinterpret_cast<const u32x4*>(mp) + i);
       it.m[4 * i + 0] = v.x; it.m[4 * i + 1] = v.y; it.m[4 * i + 2] = v.z; it.m[4 * i + 3] = v.w;
     }
   } else if constexpr (kDw == 2) {
-    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(mp));
+    const u32x2 v = ld_nt<NT>(reinterpret_cast<const u32x2*>(mp));
     it.m[0] = v.x; it.m[1] = v.y;
   } else {
-    it.m[0] = __builtin_nontemporal_load(mp);
+    it.m[0] = ld_nt<NT>(mp);
   }
 }
 
