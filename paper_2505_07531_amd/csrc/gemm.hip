@@ -545,7 +545,16 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
       if constexpr (kUni) {
         // few 128 x 64 tiles (e.g. 4096 weight rows at m <= 256): split k over the waves
         const long tiles = (long)((d->n + 127) / 128) * ((m + 63) / 64);
-        if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
+        // many rows: 128 x 48 per wave (each decoded fragment feeds 8 products) in
+        // 128 x 192 blocks, one per compute unit, where the last round of blocks keeps
+        // most units busy (11008x4096 uniform-3 at m = 512: 110 -> 91 us, m = 1024 193
+        // -> 165; 22016x4096 m = 512 183 -> 163; but 11008 rows at m = 768, two rounds
+        // with 92 blocks in the second, 166 against 167)
+        const long big = (long)((d->n + 191) / 192) * ((m + 127) / 128);
+        const long last = big % 256 == 0 ? 256 : big % 256;
+        if (QX_GEMM_CFG == 0 && m >= 384 && last >= 150)
+          launch_gemm_cfg<BITS, KIND, G, 8, 3, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
+        else if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_BIG_W == 8 && d->k > 64 * 128 && tiles <= 256)
           launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8, 8>(d, p, m, X, sx, Y, s);
