@@ -226,7 +226,7 @@ int qx_gemm_a8(const qx_desc* d, const void* packed, int32_t m, const int8_t* Xq
  *   X fp16 [m][k] row-major; Y fp16 [m][n] row-major (written; 2-byte
  *   alignment suffices for Y). fp16 products, fp32 accumulate, RNE to fp16:
  *   on the matrix cores with W' decoded exactly into their operands (for a few
- *   rows, m <= 16 by shape and format, each lane decoding its own chunks as in
+ *   rows, m <= 64 by shape and format, each lane decoding its own chunks as in
  *   the GEMV), or, for m <= 4 where that measured faster, GEMV-style with every
  *   code decoded once for all rows. m = 0 or n = 0 is a no-op; m must be
  *   <= 65536. All formats, Q4X included. Deterministic.

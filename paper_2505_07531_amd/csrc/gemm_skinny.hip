@@ -1,5 +1,5 @@
 // Small-batch quantized GEMM on the matrix cores: Y[m][n] = sum_k X[m][k] W'[n][k]
-// for 2 <= m <= 16 activation rows (decode of several sequences, short prefill chunks).
+// for 2 <= m <= 64 activation rows (decode of several sequences, short prefill chunks).
 //
 // With few activation rows the product is still bound by streaming the packed
 // weights (decoding is memory-bound, Section 2.4 of the paper), so this kernel
@@ -19,9 +19,11 @@
 //     codebook weights are table entries fetched with v_perm_b32, Q4X entries
 //     times the group's scale;
 //   * the A fragment of a piece is the 8 activations of the piece's positions in
-//     the decoder's pair order; a wave stages the m activation rows of its four
+//     the decoder's pair order; a wave stages up to 16 activation rows of its four
 //     chunks in its own LDS rows with coalesced loads and reads the fragments
-//     from there (rows past m repeat row m - 1 and are not stored);
+//     from there (rows past the tile repeat its last row and are not stored);
+//     more than 16 rows are taken as 16-row tiles in turn, the codes decoded again
+//     for each;
 //   * the W waves of a block share its 16*RF weight rows and split the chunks
 //     (wave w takes chunks 4(w + W j) .. + 3 for j < J); their 16x16 fp32 tiles are
 //     added in wave order through LDS, so results are deterministic.
@@ -188,7 +190,7 @@ constexpr int kXRow = 1024 + 16;
 // item's activation rows are loaded while the current one is multiplied.
 // LDS: W * m rows of kXRow bytes, reused at the end for the W * RF tiles of 16 x 16
 // fp32 that are added in wave order.
-template <int BITS, int KIND, int G, int RF, int J, int LB>
+template <int BITS, int KIND, int G, int RF, int J, int LB, int MT>
 __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict__ packed,
                                                          const uint16_t* __restrict__ X,
                                                          uint16_t* __restrict__ Y, int n, int k, int m) {
@@ -200,7 +202,9 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
   const int g = lane >> 4, li = lane & 15;
   const int n0 = blockIdx.x * 16 * RF;
   const DecodeConsts kc = decode_consts();
-  char* xs = lds + (size_t)wave * m * kXRow;  // this wave's activation rows
+  const int mtiles = (m + 15) >> 4, rows0 = min(m, 16);
+  char* xs = lds + (size_t)wave * rows0 * kXRow;  // this wave's activation rows (one 16-row tile)
+  float* red = reinterpret_cast<float*>(lds + (size_t)W * rows0 * kXRow);  // W * RF tiles of 16 x 16
 
   Item<BITS, KIND, G> it[J][RF];
   auto load_frag = [&](int j, int f) {  // rows and chunks clamped in bounds
@@ -208,13 +212,13 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
                                      min(4 * (wave + W * j) + g, C - 1), C, G_row);
   };
   u32x4 xv[16];
-  auto load_x = [&](int j) {  // chunks past C clamped to the last (their weights are zero)
-    const uint16_t* src = X + (size_t)min(4 * (wave + W * j) + g, C - 1) * 128 + 8 * li;
+  auto load_x = [&](int j, int mt) {  // chunks past C clamped to the last (their weights are zero)
+    const uint16_t* src = X + (size_t)16 * mt * k + (size_t)min(4 * (wave + W * j) + g, C - 1) * 128 + 8 * li;
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      if (r < m) xv[r] = *reinterpret_cast<const u32x4*>(src + (size_t)r * k);
+      if (16 * mt + r < m) xv[r] = *reinterpret_cast<const u32x4*>(src + (size_t)r * k);
   };
-  load_x(0);  // small and L2-resident: first, so that staging waits for it alone
+  load_x(0, 0);  // small and L2-resident: first, so that staging waits for it alone
   if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
   load_frag(0, 0);
   if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
@@ -228,61 +232,68 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
     __syncthreads();
   }
 
-  f4_t acc[RF];
+  // activation tiles of 16 rows in turn (at most MT), every code decoded again for each
 #pragma unroll
-  for (int f = 0; f < RF; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-
+  for (int mt = 0; mt < MT; ++mt) {
+    if (mt >= mtiles) break;
+    const int rows = min(16, m - 16 * mt);
+    f4_t acc[RF];
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    if (4 * (wave + W * j) >= C) break;  // the wave's chunks of this item are all past C
-    // stage the item's rows; the LDS instructions of one wave execute in order, so the
-    // reads below see these writes and the writes see the previous item's reads done
+    for (int f = 0; f < RF; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      if (r < m) *reinterpret_cast<u32x4*>(xs + r * kXRow + 16 * lane) = __builtin_bit_cast(u32x4, x_frag<BITS>(xv[r]));
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    h8_t a[16];
-    {
-      const char* src = xs + min(li, m - 1) * kXRow + 256 * g;
+    for (int j = 0; j < J; ++j) {
+      if (4 * (wave + W * j) >= C) break;  // the wave's chunks of this item are all past C
+      // stage the item's rows; the LDS instructions of one wave execute in order, so the
+      // reads below see these writes and the writes see the previous item's reads done
 #pragma unroll
-      for (int P = 0; P < 16; ++P) a[P] = *reinterpret_cast<const h8_t*>(src + 16 * P);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (j + 1 < J) load_x(j + 1);
-    const bool valid = 4 * (wave + W * j) + g < C;  // false only in the last item of a row
+      for (int r = 0; r < 16; ++r)
+        if (r < rows)
+          *reinterpret_cast<u32x4*>(xs + r * kXRow + 16 * lane) = __builtin_bit_cast(u32x4, x_frag<BITS>(xv[r]));
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      h8_t a[16];
+      {
+        const char* src = xs + min(li, rows - 1) * kXRow + 256 * g;
 #pragma unroll
-    for (int f = 0; f < RF; ++f) {
-      const ItemTables<BITS, KIND, G> tb = item_tables<BITS, KIND, G>(it[j][f], q4lut, valid);
+        for (int P = 0; P < 16; ++P) a[P] = *reinterpret_cast<const h8_t*>(src + 16 * P);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // the next staged rows: this tile's next item, else the next tile's first
+      if (j + 1 < J && 4 * (wave + W * (j + 1)) < C) load_x(j + 1, mt);
+      else if (mt + 1 < MT && mt + 1 < mtiles) load_x(0, mt + 1);
+      const bool valid = 4 * (wave + W * j) + g < C;  // false only in the last item of a row
+#pragma unroll
+      for (int f = 0; f < RF; ++f) {
+        const ItemTables<BITS, KIND, G> tb = item_tables<BITS, KIND, G>(it[j][f], q4lut, valid);
 #define QX_SKINNY_PIECE(P) \
   acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[P], piece_frag<BITS, KIND, G, P>(it[j][f], tb, kc), acc[f], 0, 0, 0);
-      QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
-      QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
-      QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
-      QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
+        QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
+        QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
+        QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
+        QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
 #undef QX_SKINNY_PIECE
+      }
     }
-  }
 
-  // wave tiles -> LDS (every wave is past its last read of its rows): red[(w * RF + f) * 256
-  // + 4 * lane + r] holds D[4 g + r][li]
-  __syncthreads();
-  float* red = reinterpret_cast<float*>(lds);
+    // wave tiles -> LDS: red[(w * RF + f) * 256 + 4 * lane + r] holds D[4 g + r][li]; the
+    // barrier before also separates these writes from the previous tile's sums
+    __syncthreads();
 #pragma unroll
-  for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(red + (wave * RF + f) * 256 + 4 * lane) = acc[f];
-  __syncthreads();
-  // output (row r of Y, column c) = tile f = c / 16, element D[r][c % 16]:
-  // lane 16 (r / 4) + c % 16, register r % 4; waves added in order
-  for (int o = threadIdx.x; o < 256 * RF; o += blockDim.x) {
-    const int c = o % (16 * RF), r = o / (16 * RF);
-    const int f = c >> 4;
-    const int idx = f * 256 + 4 * (16 * (r >> 2) + (c & 15)) + (r & 3);
-    float s = 0.f;
-    for (int w = 0; w < W; ++w) s += red[w * RF * 256 + idx];
-    if (r < m && n0 + c < n) Y[(size_t)r * n + n0 + c] = (uint16_t)float_to_half_bits(s);
+    for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(red + (wave * RF + f) * 256 + 4 * lane) = acc[f];
+    __syncthreads();
+    // output (row 16 mt + r of Y, column c) = tile f = c / 16, element D[r][c % 16]:
+    // lane 16 (r / 4) + c % 16, register r % 4; waves added in order
+    for (int o = threadIdx.x; o < 256 * RF; o += blockDim.x) {
+      const int c = o % (16 * RF), r = o / (16 * RF);
+      const int f = c >> 4;
+      const int idx = f * 256 + 4 * (16 * (r >> 2) + (c & 15)) + (r & 3);
+      float s = 0.f;
+      for (int w = 0; w < W; ++w) s += red[w * RF * 256 + idx];
+      if (r < rows && n0 + c < n) Y[(size_t)(16 * mt + r) * n + n0 + c] = (uint16_t)float_to_half_bits(s);
+    }
   }
 }
 
@@ -290,11 +301,15 @@ template <int BITS, int KIND, int G, int RF, int J, int LB>
 int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
   const int C = d->k / 128;
   const int W = (C + 4 * J - 1) / (4 * J);
-  if (W > LB / 64) return QX_E_UNSUPPORTED;
-  const size_t lds = std::max((size_t)W * m * kXRow, (size_t)W * RF * 256 * sizeof(float));
+  if (W > LB / 64 || m > 64) return QX_E_UNSUPPORTED;
+  const size_t lds = (size_t)W * std::min(m, 16) * kXRow + (size_t)W * RF * 256 * sizeof(float);
   const unsigned blocks = (unsigned)((d->n + 16 * RF - 1) / (16 * RF));
-  hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB>), dim3(blocks), dim3(64 * W), lds, s, p, X, Y,
-                     d->n, d->k, m);
+  if (m <= 16)
+    hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB, 1>), dim3(blocks), dim3(64 * W), lds, s, p, X,
+                       Y, d->n, d->k, m);
+  else
+    hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB, 4>), dim3(blocks), dim3(64 * W), lds, s, p, X,
+                       Y, d->n, d->k, m);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 
@@ -314,7 +329,7 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
   // tall matrices: three weight-row fragments per wave with one item per lane, two with
   // two (the registers of three spill in some formats), one beyond
   const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : (d->n >= 8192 ? (J == 1 ? 3 : J == 2 ? 2 : 1) : 1);
-  if (m < 1 || m > 16) return QX_E_UNSUPPORTED;
+  if (m < 1 || m > QX_SKINNY_MAX_M) return QX_E_UNSUPPORTED;
 #define QX_SKINNY_J(JJ)                                                                                   \
   case JJ:                                                                                                \
     return rf >= 3   ? launch_cfg<BITS, KIND, G, (JJ <= 2 ? 3 : 4 - JJ / 2), JJ, LB>(d, p, m, X, Y, s)   \
@@ -329,7 +344,13 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
 
 }  // namespace
 
-// Whether qx_gemm runs m rows on this kernel. Measured against the small-batch GEMV-style
+// Whether qx_gemm runs m rows on this kernel. Beyond 16 rows (several activation tiles,
+// every code decoded again per tile) only rows of at most 32 chunks with one round of
+// blocks (us at m = 24 / 32 / 48 / 64 against the matrix-core GEMM: 11008x4096 uniform-3
+// g64 15.2 / 15.7 / 21.0 / 26.5 vs 22.1 / 21.8 / 27.6 / 27.1; 4096x4096 codebook-3 7.5 /
+// 7.9 / 10.1 / 12.4 vs 14.0 / 14.4 / 14.7 / 14.5; 22016 rows, two rounds: 28.5 / 30.2 /
+// 40.2 / 49.7 vs 24.5 / 24.9 / 40.1 / 41.4). Up to 16 rows: measured against the
+// small-batch GEMV-style
 // kernel (m <= 4) and the matrix-core GEMM on 11008x4096, 4096x11008 and 4096x4096 in all
 // thirteen formats at m = 2-16 (us, 3-bit uniform g64 at m = 2 / 8 / 16: 11008x4096 8.4 /
 // 9.0 / 9.9 against 9.2 / 15.7 / 15.8; 4096x11008 10.9 / 12.9 / 14.6 against 10.8 / 16.2 /
@@ -340,10 +361,14 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
 bool gemm_skinny_applies(const qx_desc* d, int m) {
   const int C = d->k / 128, J = (C + 31) / 32;  // items per lane (8 waves of 4 chunks)
 #ifdef QX_SKINNY_FORCE
-  return m >= 2 && m <= 16 && J <= 4;
+  return m >= 2 && m <= QX_SKINNY_MAX_M && J <= 4;
 #endif
   if (m < 2 || m > QX_SKINNY_MAX_M || J > 4) return false;
   const bool cb = d->kind == QX_CODEBOOK, q4x = d->kind == QX_Q4X;
+  if (m > 16) {  // 16-row activation tiles in turn, every code decoded again for each
+    const int rf = d->n >= 8192 ? 3 : 1;
+    return J == 1 && (d->n + 16 * rf - 1) / (16 * rf) <= 256 && !q4x && !(cb && d->bits == 4 && d->group <= 64);
+  }
   if (cb && d->bits == 4) return d->group >= 64 && J == 1;
   if (q4x) return J == 1 && (m >= 3 || d->n <= 4096);
   if (J >= 2 && m == 2) return cb && d->group >= 64;

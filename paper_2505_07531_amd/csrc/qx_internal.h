@@ -64,7 +64,7 @@ int launch_gemv_multi(const qx_desc* d, const void* packed, int m, const uint16_
 // chunk-per-lane loads (gemm_skinny.hip; gemm_skinny_applies picks it per shape and
 // format); k up to 128 chunks.
 #ifndef QX_SKINNY_MAX_M
-#define QX_SKINNY_MAX_M 16
+#define QX_SKINNY_MAX_M 64
 #endif
 bool gemm_skinny_applies(const qx_desc* d, int m);
 

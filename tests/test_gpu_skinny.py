@@ -1,10 +1,11 @@
-"""Parity of the small-batch matrix-core GEMM (qx_gemm at 2 <= m <= 16) with the oracle.
+"""Parity of the small-batch matrix-core GEMM (qx_gemm at 2 <= m <= 64) with the oracle.
 
 That kernel keeps the GEMV's one-chunk-per-lane loads and multiplies on the
 matrix cores: a block's waves split each row's chunks 4 per wave and item (up
 to 4 items per lane, up to 8 waves) on 16, 32 or 48 weight rows per block (one,
 two or three row fragments per wave), each wave stages the m activation rows of
-its chunks in LDS, and the m rows fill one 16-row tile. The cases below take
+its chunks in LDS, and the m rows fill 16-row tiles taken in turn (more than one
+only on rows of at most 32 chunks). The cases below take
 each of those launch shapes at an m and shape that qx_gemm routes to it, with
 ragged rows, chunk slots past the end of a row, waves without a last item and
 padded activation rows, in all thirteen formats (where a format is routed
@@ -38,6 +39,10 @@ CASES = [
     (16, 8200, 4096),   # the same at a full activation tile
     (7, 8193, 5120),    # C = 40: two row fragments per wave and 2 items; one row in the last block
     (6, 60, 16384),     # C = 128: 4 items, 8 waves
+    (24, 130, 4096),    # two activation tiles, the second of 8 rows
+    (33, 8200, 4096),   # three tiles (the last of one row), three row fragments per wave
+    (64, 40, 384),      # four full tiles, one wave
+    (47, 8193, 1152),   # three tiles, three fragments, one row in the last block
     (3, 20, 22016),     # C = 172: past the kernel's rows, routed elsewhere
     (4, 33, 32768),     # C = 256: routed elsewhere
 ]
@@ -88,12 +93,13 @@ def test_skinny_matches_oracle(gpu, fmt, case):
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
-@pytest.mark.parametrize("m,n,k", [(4, 8200, 11008), (6, 4000, 11008), (16, 8200, 4096)],
-                         ids=["m4_8200x11008", "m6_4000x11008", "m16_8200x4096"])
+@pytest.mark.parametrize("m,n,k", [(4, 8200, 11008), (6, 4000, 11008), (16, 8200, 4096), (40, 4096, 4096)],
+                         ids=["m4_8200x11008", "m6_4000x11008", "m16_8200x4096", "m40_4096x4096"])
 def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n, k):
     """Activation row r one-hot at position j_r: row r of Y equals column j_r of W' in
     value (a sum that starts at +0 turns -0 weights into +0), on shapes with 3 items per
-    lane and a ragged last item (16-row blocks), and with 48-row blocks at m = 16."""
+    lane and a ragged last item (16-row blocks), with 48-row blocks at m = 16, and with three
+    activation tiles at m = 40."""
     qx = gpu
     q = _quant(n, k, fmt, seed=m)
     cols = np.random.default_rng(m + 1).choice(k, m, replace=False)
@@ -104,7 +110,7 @@ def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n, k):
     assert np.array_equal(Y.astype(np.float32), ref.astype(np.float32))
 
 
-@pytest.mark.parametrize("m", [2, 6, 8, 13, 16])
+@pytest.mark.parametrize("m", [2, 6, 8, 13, 16, 40])
 def test_skinny_rows_equal_gemv(gpu, m):
     """Each row of the product against the batch-1 GEMV of the same row (two different
     fp32 summation orders of the same products)."""
