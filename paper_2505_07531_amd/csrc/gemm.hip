@@ -501,6 +501,12 @@ static void launch_gemm_cfg(const qx_desc* d, const char* p, int m, const void* 
 // 61.8, but 112.7 -> 120.3 at m = 512, 512 tiles); 4 keeps the 4-wave shapes
 #define QX_GEMM_BIG_W 8
 #endif
+#ifndef QX_GEMM_BIG_S
+#define QX_GEMM_BIG_S 4  // super-round (rounds per code load) of the 128 x 192 blocks
+#endif
+#ifndef QX_GEMM_BIG_DX
+#define QX_GEMM_BIG_DX 1  // activation rounds in flight of the 128 x 192 blocks (11008x4096 u3g64 m = 512: 95.1 us with 2, 89.8 with 1)
+#endif
 #ifndef QX_GEMM_SMALL_W
 #define QX_GEMM_SMALL_W 4  // 4: waves per block for m <= 16 by shape; 8, 16 force (sweeps)
 #endif
@@ -553,7 +559,7 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
         const long big = (long)((d->n + 191) / 192) * ((m + 127) / 128);
         const long last = big % 256 == 0 ? 256 : big % 256;
         if (QX_GEMM_CFG == 0 && m >= 384 && last >= 150)
-          launch_gemm_cfg<BITS, KIND, G, 8, 3, 1, 4, 2, A8>(d, p, m, X, sx, Y, s);
+          launch_gemm_cfg<BITS, KIND, G, 8, 3, 1, QX_GEMM_BIG_S, QX_GEMM_BIG_DX, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_BIG_W == 8 && d->k > 64 * 128 && tiles <= 256)

@@ -177,19 +177,22 @@ constexpr int kXRow = 1024 + 16;
 
 // Block: W = blockDim.x / 64 waves on weight rows n0 .. n0 + 16 RF - 1. Lane l of
 // wave w: column (weight row) n0 + 16 f + l % 16 of fragment f, chunk
-// 4 (w + W j) + l / 16 of item j, activation row l % 16 (rows past m repeat row m - 1).
+// 4 (w + W j) + l / 16 of item j, activation row 16 mt + l % 16 of tile mt (rows past
+// the tile's last repeat it). Up to MT tiles of 16 activation rows are taken in turn;
+// the codes stay in registers and are decoded again for each tile.
 //
-// Activations: the m rows of an item's four chunks are m contiguous 1 KB runs, so the
+// Activations: the rows of an item's four chunks are contiguous 1 KB runs, so the
 // wave loads each run with one fully coalesced 16-byte-per-lane load (lane l: chunk
 // l / 16, piece l % 16), permutes it into the decoders' pair order and writes it to its
 // own LDS rows; each lane then reads its 16 A fragments (row l % 16, chunk l / 16)
 // from there. Reading the fragments straight from X would touch 64 cache lines per
 // load instead of 8.
-// Loads are issued in the order the products consume them: item 0's activation rows,
-// the first weight-row fragment of item 0, the other fragments and items; the next
-// item's activation rows are loaded while the current one is multiplied.
-// LDS: W * m rows of kXRow bytes, reused at the end for the W * RF tiles of 16 x 16
-// fp32 that are added in wave order.
+// Loads are issued in the order the products consume them: the first tile's
+// activation rows of item 0, the first weight-row fragment of item 0, the other
+// fragments and items; the next staged rows (next item, else next tile) are loaded
+// while the current ones are multiplied.
+// LDS: W * min(m, 16) rows of kXRow bytes, then the W * RF tiles of 16 x 16 fp32 that
+// are added in wave order after each activation tile.
 template <int BITS, int KIND, int G, int RF, int J, int LB, int MT>
 __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict__ packed,
                                                          const uint16_t* __restrict__ X,
