@@ -191,8 +191,8 @@ constexpr int kXRow = 1024 + 16;
 // activation rows of item 0, the first weight-row fragment of item 0, the other
 // fragments and items; the next staged rows (next item, else next tile) are loaded
 // while the current ones are multiplied.
-// LDS: W * min(m, 16) rows of kXRow bytes, then the W * RF tiles of 16 x 16 fp32 that
-// are added in wave order after each activation tile.
+// LDS: W * min(m, 16) rows of kXRow bytes, reused after each activation tile for the
+// W * RF tiles of 16 x 16 fp32 that are added in wave order.
 template <int BITS, int KIND, int G, int RF, int J, int LB, int MT>
 __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict__ packed,
                                                          const uint16_t* __restrict__ X,
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
   const DecodeConsts kc = decode_consts();
   const int mtiles = (m + 15) >> 4, rows0 = min(m, 16);
   char* xs = lds + (size_t)wave * rows0 * kXRow;  // this wave's activation rows (one 16-row tile)
-  float* red = reinterpret_cast<float*>(lds + (size_t)W * rows0 * kXRow);  // W * RF tiles of 16 x 16
+  float* red = reinterpret_cast<float*>(lds);      // W * RF tiles of 16 x 16, over the staged rows
 
   Item<BITS, KIND, G> it[J][RF];
   auto load_frag = [&](int j, int f) {  // rows and chunks clamped in bounds
@@ -281,8 +281,8 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
       }
     }
 
-    // wave tiles -> LDS: red[(w * RF + f) * 256 + 4 * lane + r] holds D[4 g + r][li]; the
-    // barrier before also separates these writes from the previous tile's sums
+    // wave tiles -> LDS over the staged rows (every wave is past its reads of them):
+    // red[(w * RF + f) * 256 + 4 * lane + r] holds D[4 g + r][li]
     __syncthreads();
 #pragma unroll
     for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(red + (wave * RF + f) * 256 + 4 * lane) = acc[f];
@@ -297,6 +297,7 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
       for (int w = 0; w < W; ++w) s += red[w * RF * 256 + idx];
       if (r < rows && n0 + c < n) Y[(size_t)(16 * mt + r) * n + n0 + c] = (uint16_t)float_to_half_bits(s);
     }
+    if (mt + 1 < mtiles) __syncthreads();  // the sums are read before the next tile is staged
   }
 }
 
@@ -305,7 +306,7 @@ int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16
   const int C = d->k / 128;
   const int W = (C + 4 * J - 1) / (4 * J);
   if (W > LB / 64 || m > 64) return QX_E_UNSUPPORTED;
-  const size_t lds = (size_t)W * std::min(m, 16) * kXRow + (size_t)W * RF * 256 * sizeof(float);
+  const size_t lds = std::max((size_t)W * std::min(m, 16) * kXRow, (size_t)W * RF * 256 * sizeof(float));
   const unsigned blocks = (unsigned)((d->n + 16 * RF - 1) / (16 * RF));
   if (m <= 16)
     hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB, 1>), dim3(blocks), dim3(64 * W), lds, s, p, X,
@@ -319,6 +320,9 @@ int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16
 #ifndef QX_SKINNY_RF
 #define QX_SKINNY_RF 0  // 0: by shape; 1, 2, 3 force the weight-row fragments per wave
 #endif
+#ifndef QX_SKINNY_RF6_ROWS
+#define QX_SKINNY_RF6_ROWS 16384  // rows from which one-item lanes take six weight-row fragments
+#endif
 #ifndef QX_SKINNY_LB
 #define QX_SKINNY_LB 512  // threads per block at most (8 waves: up to 256 VGPRs per lane)
 #endif
@@ -331,11 +335,14 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
   const int J = (C + 4 * WMAX - 1) / (4 * WMAX);  // items per lane
   // tall matrices: three weight-row fragments per wave with one item per lane, two with
   // two (the registers of three spill in some formats), one beyond
-  const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : (d->n >= 8192 ? (J == 1 ? 3 : J == 2 ? 2 : 1) : 1);
+  const bool six = d->n >= QX_SKINNY_RF6_ROWS && J == 1 && m <= 16 &&
+                   !(KIND == QX_CODEBOOK && BITS == 4 && G <= 64);  // their tables spill at six
+  const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : six ? 6 : d->n >= 8192 ? (J == 1 ? 3 : J == 2 ? 2 : 1) : 1;
   if (m < 1 || m > QX_SKINNY_MAX_M) return QX_E_UNSUPPORTED;
 #define QX_SKINNY_J(JJ)                                                                                   \
   case JJ:                                                                                                \
-    return rf >= 3   ? launch_cfg<BITS, KIND, G, (JJ <= 2 ? 3 : 4 - JJ / 2), JJ, LB>(d, p, m, X, Y, s)   \
+    return rf >= 6 && JJ == 1 ? launch_cfg<BITS, KIND, G, 6, 1, LB>(d, p, m, X, Y, s)                \
+           : rf >= 3 ? launch_cfg<BITS, KIND, G, (JJ <= 2 ? 3 : 4 - JJ / 2), JJ, LB>(d, p, m, X, Y, s)   \
            : rf == 2 ? launch_cfg<BITS, KIND, G, (JJ <= 3 ? 2 : 1), JJ, LB>(d, p, m, X, Y, s)             \
                      : launch_cfg<BITS, KIND, G, 1, JJ, LB>(d, p, m, X, Y, s);
   switch (J) {

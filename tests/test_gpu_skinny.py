@@ -2,8 +2,8 @@
 
 That kernel keeps the GEMV's one-chunk-per-lane loads and multiplies on the
 matrix cores: a block's waves split each row's chunks 4 per wave and item (up
-to 4 items per lane, up to 8 waves) on 16, 32 or 48 weight rows per block (one,
-two or three row fragments per wave), each wave stages the m activation rows of
+to 4 items per lane, up to 8 waves) on 16, 32, 48 or 96 weight rows per block
+(one, two, three or six row fragments per wave), each wave stages the m activation rows of
 its chunks in LDS, and the m rows fill 16-row tiles taken in turn (more than one
 only on rows of at most 32 chunks). The cases below take
 each of those launch shapes at an m and shape that qx_gemm routes to it, with
@@ -43,6 +43,7 @@ CASES = [
     (33, 8200, 4096),   # three tiles (the last of one row), three row fragments per wave
     (64, 40, 384),      # four full tiles, one wave
     (47, 8193, 1152),   # three tiles, three fragments, one row in the last block
+    (9, 16400, 1024),   # six row fragments per wave (16384 rows or more), last block of 80 rows
     (3, 20, 22016),     # C = 172: past the kernel's rows, routed elsewhere
     (4, 33, 32768),     # C = 256: routed elsewhere
 ]
