@@ -30,7 +30,18 @@
 //
 // RF weight-row fragments share each A fragment: tall matrices take three per
 // wave, which puts one block on nearly every compute unit of an 11008-row matrix.
+// That form loads all its codes before its first product, so each compute unit
+// streams only until its one block has its data. Where a compute unit holds fewer rows
+// in the pipelined form below (one block per compute unit, activations staged once, two
+// 16-row groups in flight per wave while the previous one is multiplied), or four
+// groups or more, rows of at most 32 chunks at m <= 16 take that form (22016x4096
+// uniform-4 g128 at m = 2 / 16: 16.0 / 17.6 us -> 13.8 / 15.2; 16400x4096 uniform-3 g64
+// 13.6 / 15.3 -> 10.8 / 12.2; 8192x4096 7.9 / 9.3 -> 7.0 / 8.5; 11008 and 12288 rows,
+// 48 rows per compute unit in both forms: the one-shot form measured equal or faster).
 // qx_gemm routes m rows here where it measured faster (gemm_skinny_applies).
+#include <atomic>
+#include <utility>
+
 #include "gemv_common.h"
 
 namespace qx {
@@ -301,6 +312,184 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
   }
 }
 
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(0), f(1), .., f(N - 1) with compile-time arguments
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Products of one group of RF weight-row fragments with the A fragments held in
+// registers: acc[f] = sum over the lane's 16 pieces.
+template <int BITS, int KIND, int G, int RF>
+__device__ __forceinline__ void mul_group(const Item<BITS, KIND, G> (&it)[RF], const h8_t (&a)[16],
+                                          const uint32_t* q4lut, bool valid, const DecodeConsts& kc,
+                                          f4_t (&acc)[RF]) {
+#pragma unroll
+  for (int f = 0; f < RF; ++f) {
+    acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+    const ItemTables<BITS, KIND, G> tb = item_tables<BITS, KIND, G>(it[f], q4lut, valid);
+#define QX_SKINNY_PIECE(P) \
+  acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[P], piece_frag<BITS, KIND, G, P>(it[f], tb, kc), acc[f], 0, 0, 0);
+    QX_SKINNY_PIECE(0) QX_SKINNY_PIECE(1) QX_SKINNY_PIECE(2) QX_SKINNY_PIECE(3)
+    QX_SKINNY_PIECE(4) QX_SKINNY_PIECE(5) QX_SKINNY_PIECE(6) QX_SKINNY_PIECE(7)
+    QX_SKINNY_PIECE(8) QX_SKINNY_PIECE(9) QX_SKINNY_PIECE(10) QX_SKINNY_PIECE(11)
+    QX_SKINNY_PIECE(12) QX_SKINNY_PIECE(13) QX_SKINNY_PIECE(14) QX_SKINNY_PIECE(15)
+#undef QX_SKINNY_PIECE
+  }
+}
+
+// Pipelined form for rows of 29-32 chunks (one item per lane, all 8 waves busy) and
+// m <= 16, on matrices of at least NB groups of 16 RF weight rows per compute unit: one
+// block of 8 waves per compute unit stages the activations once and keeps each lane's 16
+// A fragments in registers, then takes groups blockIdx.x, blockIdx.x + gridDim.x, ... in
+// turn (the chip reads one band of rows at a time). Each wave keeps the codes of NB
+// groups in flight: those of group s + NB are requested once group s is multiplied, so
+// the decode and products of one group overlap the arrival of the next. The waves do not
+// wait for each other: each writes its fp32 tile of group s to its own LDS slot, and
+// after one barrier the block adds the slots in wave order and stores its rows. Rows of
+// the last group past n repeat row n - 1; no load reaches past the block's last group.
+template <int BITS, int KIND, int G, int RF, int NB>
+__global__ __launch_bounds__(512) void gemm_skinny_loop_kernel(const char* __restrict__ packed,
+                                                               const uint16_t* __restrict__ X,
+                                                               uint16_t* __restrict__ Y, int n, int k, int m) {
+  constexpr int W = 8;
+  extern __shared__ __align__(16) char lds[];
+  __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
+  const int C = k >> 7, G_row = k / G;
+  const size_t meta_off = (size_t)n * k * BITS / 8;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g = lane >> 4, li = lane & 15;
+  const int rows = min(m, 16);
+  const int groups = (n + 16 * RF - 1) / (16 * RF);
+  const int steps = (groups - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;  // groups of this block
+  const int c = min(4 * wave + g, C - 1);
+  const bool valid = 4 * wave + g < C;
+  const DecodeConsts kc = decode_consts();
+
+  Item<BITS, KIND, G> it[NB][RF];
+  auto load_grp = [&](Item<BITS, KIND, G>(&dst)[RF], int s) {  // group blockIdx.x + s gridDim.x
+    const int n0 = ((int)blockIdx.x + s * (int)gridDim.x) * 16 * RF;
+#pragma unroll
+    for (int f = 0; f < RF; ++f)
+      load_item<BITS, KIND, G, true>(dst[f], packed, meta_off, min(n0 + 16 * f + li, n - 1), c, C, G_row);
+  };
+  u32x4 xv[16];
+  {
+    const uint16_t* src = X + (size_t)c * 128 + 8 * li;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (r < rows) xv[r] = *reinterpret_cast<const u32x4*>(src + (size_t)r * k);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    load_grp(it[b], b);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (KIND == QX_Q4X) stage_q4x_lut(packed, n, k, q4lut);
+
+  h8_t a[16];
+  {
+    char* xs = lds + (size_t)wave * rows * kXRow;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (r < rows) *reinterpret_cast<u32x4*>(xs + r * kXRow + 16 * lane) = __builtin_bit_cast(u32x4, x_frag<BITS>(xv[r]));
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const char* src = xs + min(li, rows - 1) * kXRow + 256 * g;
+#pragma unroll
+    for (int P = 0; P < 16; ++P) a[P] = *reinterpret_cast<const h8_t*>(src + 16 * P);
+  }
+  __syncthreads();  // every wave holds its fragments (and the Q4X tables are staged)
+
+  // wave tiles of group s at red[(s * W + wave) * RF * 256 ..], over the staged rows;
+  // the waves run through their groups without waiting for each other
+  float* red = reinterpret_cast<float*>(lds);
+  auto product = [&](const Item<BITS, KIND, G>(&cur)[RF], int st) {
+    f4_t acc[RF];
+    mul_group<BITS, KIND, G, RF>(cur, a, q4lut, valid, kc, acc);
+    float* rd = red + (st * W + wave) * RF * 256;
+#pragma unroll
+    for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(rd + f * 256 + 4 * lane) = acc[f];
+  };
+  // Full rounds: group s0 + b, then the load of group s0 + b + NB into its registers.
+  // The rest (NB + e groups, 0 <= e < NB) runs as straight-line code for each e, so that
+  // every wait before a group's products leaves the later groups' loads in flight and no
+  // load reaches past the block's last group.
+  int s0 = 0;
+  for (; s0 + 2 * NB <= steps; s0 += NB) {
+    static_for<NB>([&](auto b) {
+      product(it[b], s0 + b);
+      __builtin_amdgcn_sched_barrier(0);
+      load_grp(it[b], s0 + b + NB);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  }
+  const int e = steps - s0 - NB;  // 0 <= e < NB (the launch gives every block NB groups or more)
+  static_for<NB>([&](auto E) {
+    if (e == E) {
+      static_for<NB>([&](auto b) {
+        product(it[b], s0 + b);
+        if constexpr (b < E) {
+          __builtin_amdgcn_sched_barrier(0);
+          load_grp(it[b], s0 + b + NB);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+      static_for<E>([&](auto b) { product(it[b], s0 + NB + b); });
+    }
+  });
+  __syncthreads();
+  // output (row r of Y, column n0 + cc of group s) = tile f = cc / 16, element D[r][cc % 16]:
+  // lane 16 (r / 4) + cc % 16, register r % 4; waves added in order
+  for (int o = threadIdx.x; o < steps * 256 * RF; o += 64 * W) {
+    const int st = o / (256 * RF), oo = o % (256 * RF);
+    const int cc = oo % (16 * RF), r = oo / (16 * RF);
+    const int f = cc >> 4;
+    const int idx = f * 256 + 4 * (16 * (r >> 2) + (cc & 15)) + (r & 3);
+    const float* rd = red + st * W * RF * 256;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < W; ++w) sum += rd[w * RF * 256 + idx];
+    const int n0 = ((int)blockIdx.x + st * (int)gridDim.x) * 16 * RF;
+    if (r < rows && n0 + cc < n) Y[(size_t)r * n + n0 + cc] = (uint16_t)float_to_half_bits(sum);
+  }
+}
+
+#ifndef QX_SKINNY_LOOP
+#define QX_SKINNY_LOOP 1  // 0: the one-shot form only
+#endif
+
+// Compute units of the current device (cached per device).
+inline int compute_units() {
+  static std::atomic<int> cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int v = cus[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cus[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
+
+template <int BITS, int KIND, int G, int RF, int NB>
+int launch_loop(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
+  const int groups = (d->n + 16 * RF - 1) / (16 * RF), blocks = compute_units();
+  const int steps = (groups + blocks - 1) / blocks;
+  if (groups / blocks < NB || m > 16 || d->k / 128 > 32) return QX_E_UNSUPPORTED;  // every block holds NB groups
+  const size_t lds = std::max((size_t)8 * std::min(m, 16) * kXRow, (size_t)steps * 8 * RF * 256 * sizeof(float));
+  if (lds > 160 * 1024) return QX_E_UNSUPPORTED;
+  hipLaunchKernelGGL((gemm_skinny_loop_kernel<BITS, KIND, G, RF, NB>), dim3((unsigned)blocks), dim3(512), lds, s, p, X, Y,
+                     d->n, d->k, m);
+  return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
+}
+
 template <int BITS, int KIND, int G, int RF, int J, int LB>
 int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
   const int C = d->k / 128;
@@ -339,6 +528,14 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
                    !(KIND == QX_CODEBOOK && BITS == 4 && G <= 64);  // their tables spill at six
   const int rf = QX_SKINNY_RF ? QX_SKINNY_RF : six ? 6 : d->n >= 8192 ? (J == 1 ? 3 : J == 2 ? 2 : 1) : 1;
   if (m < 1 || m > QX_SKINNY_MAX_M) return QX_E_UNSUPPORTED;
+  if (QX_SKINNY_LOOP && J == 1 && m <= 16 && C > 28) {
+    // pipelined form where it holds fewer rows per compute unit than a block of the
+    // one-shot form, or four groups or more (measured; see the kernel's comment)
+    const int groups = (d->n + 15) / 16, cus = compute_units();
+    const int steps = (groups + cus - 1) / cus;
+    if (groups / cus >= 2 && steps <= 20 && (steps < rf || steps >= 4))
+      return launch_loop<BITS, KIND, G, 1, 2>(d, p, m, X, Y, s);
+  }
 #define QX_SKINNY_J(JJ)                                                                                   \
   case JJ:                                                                                                \
     return rf >= 6 && JJ == 1 ? launch_cfg<BITS, KIND, G, 6, 1, LB>(d, p, m, X, Y, s)                \

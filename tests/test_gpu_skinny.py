@@ -5,7 +5,9 @@ matrix cores: a block's waves split each row's chunks 4 per wave and item (up
 to 4 items per lane, up to 8 waves) on 16, 32, 48 or 96 weight rows per block
 (one, two, three or six row fragments per wave), each wave stages the m activation rows of
 its chunks in LDS, and the m rows fill 16-row tiles taken in turn (more than one
-only on rows of at most 32 chunks). The cases below take
+only on rows of at most 32 chunks). Tall matrices with rows of 29-32 chunks at m <= 16
+take a pipelined form instead (one block per compute unit walking 16-row groups with
+two in flight). The cases below take
 each of those launch shapes at an m and shape that qx_gemm routes to it, with
 ragged rows, chunk slots past the end of a row, waves without a last item and
 padded activation rows, in all thirteen formats (where a format is routed
@@ -44,6 +46,9 @@ CASES = [
     (64, 40, 384),      # four full tiles, one wave
     (47, 8193, 1152),   # three tiles, three fragments, one row in the last block
     (9, 16400, 1024),   # six row fragments per wave (16384 rows or more), last block of 80 rows
+    (2, 8190, 4096),    # pipelined form: two 16-row groups per compute unit, the last of 14 rows
+    (16, 16390, 3840),  # pipelined, C = 30 (lane groups past the row), 4-5 groups per block, last of 6 rows
+    (7, 22001, 4096),   # pipelined, 5-6 groups per block (both tails), the last of one row
     (3, 20, 22016),     # C = 172: past the kernel's rows, routed elsewhere
     (4, 33, 32768),     # C = 256: routed elsewhere
 ]
@@ -66,10 +71,13 @@ def _quant(n, k, fmt, seed):
     return random_quant(n, k, bits, g, kind, seed=seed)
 
 
-def _w16(q):
-    if q.kind == 2:
-        return q4x.dequant(q.codes, q.scales, q.selectors, q.codebook)
-    return oracle.dequant(q.codes, q.group, q.kind, q.scales, q.zeros, q.codebook)
+def _w16(q, rows=None):
+    """W' (fp16 values) of all rows, or of the given rows only."""
+    def sel(a):
+        return a if a is None or rows is None else a[rows]
+    if q.kind == 2:  # the codebook is per matrix
+        return q4x.dequant(sel(q.codes), sel(q.scales), sel(q.selectors), q.codebook)
+    return oracle.dequant(sel(q.codes), q.group, q.kind, sel(q.scales), sel(q.zeros), sel(q.codebook))
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
@@ -82,10 +90,9 @@ def test_skinny_matches_oracle(gpu, fmt, case):
     X = activations(k, seed=m + 7, m=m)
     pw = qx.PackedWeight.from_quant(q)
     Y = pw.gemm(to_dev(X)).cpu().numpy()
-    w16 = _w16(q)
     rows = np.arange(n) if n <= 1024 else np.sort(np.random.default_rng(m).choice(n, 1024, replace=False))
     rows = np.union1d(rows, [n - 1])  # the ragged last block
-    ref = oracle.gemm(X, w16[rows])
+    ref = oracle.gemm(X, _w16(q, rows))
     for r in range(m):
         err = oracle.normwise_rel_err(Y[r][rows], ref[r])
         assert err <= TOL, (r, err)
@@ -94,13 +101,14 @@ def test_skinny_matches_oracle(gpu, fmt, case):
 
 
 @pytest.mark.parametrize("fmt", FORMATS, ids=_fmt_id)
-@pytest.mark.parametrize("m,n,k", [(4, 8200, 11008), (6, 4000, 11008), (16, 8200, 4096), (40, 4096, 4096)],
-                         ids=["m4_8200x11008", "m6_4000x11008", "m16_8200x4096", "m40_4096x4096"])
+@pytest.mark.parametrize("m,n,k", [(4, 8200, 11008), (6, 4000, 11008), (16, 8200, 4096), (40, 4096, 4096),
+                                   (5, 16400, 4096)],
+                         ids=["m4_8200x11008", "m6_4000x11008", "m16_8200x4096", "m40_4096x4096", "m5_16400x4096"])
 def test_skinny_one_hot_rows_are_columns(gpu, fmt, m, n, k):
     """Activation row r one-hot at position j_r: row r of Y equals column j_r of W' in
     value (a sum that starts at +0 turns -0 weights into +0), on shapes with 3 items per
-    lane and a ragged last item (16-row blocks), with 48-row blocks at m = 16, and with three
-    activation tiles at m = 40."""
+    lane and a ragged last item (16-row blocks), with 48-row blocks at m = 16, with three
+    activation tiles at m = 40, and in the pipelined form (16400 rows)."""
     qx = gpu
     q = _quant(n, k, fmt, seed=m)
     cols = np.random.default_rng(m + 1).choice(k, m, replace=False)
