@@ -185,6 +185,9 @@ constexpr int kXRow = 1024 + 16;
 #ifndef QX_SKINNY_PIN
 #define QX_SKINNY_PIN 1
 #endif
+#ifndef QX_SKINNY_AHEAD
+#define QX_SKINNY_AHEAD 1  // items whose codes are requested before the first product
+#endif
 
 // Block: W = blockDim.x / 64 waves on weight rows n0 .. n0 + 16 RF - 1. Lane l of
 // wave w: column (weight row) n0 + 16 f + l % 16 of fragment f, chunk
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
   load_frag(0, 0);
   if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int j = 0; j < J; ++j)
+  for (int j = 0; j < (J < QX_SKINNY_AHEAD ? J : QX_SKINNY_AHEAD); ++j)
 #pragma unroll
     for (int f = j == 0 ? 1 : 0; f < RF; ++f) load_frag(j, f);
   if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
@@ -275,9 +278,17 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // the next staged rows: this tile's next item, else the next tile's first
+      // the next staged rows: this tile's next item, else the next tile's first; then the
+      // codes QX_SKINNY_AHEAD items ahead, so that each item's rows wait in the wave's
+      // in-order returns only behind the codes of the items before it
       if (j + 1 < J && 4 * (wave + W * (j + 1)) < C) load_x(j + 1, mt);
       else if (mt + 1 < MT && mt + 1 < mtiles) load_x(0, mt + 1);
+      if (mt == 0 && j + QX_SKINNY_AHEAD < J) {
+        if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int f = 0; f < RF; ++f) load_frag(j + QX_SKINNY_AHEAD, f);
+      }
+      if (QX_SKINNY_PIN) __builtin_amdgcn_sched_barrier(0);
       const bool valid = 4 * (wave + W * j) + g < C;  // false only in the last item of a row
 #pragma unroll
       for (int f = 0; f < RF; ++f) {
@@ -557,14 +568,19 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
 // g64 15.2 / 15.7 / 21.0 / 26.5 vs 22.1 / 21.8 / 27.6 / 27.1; 4096x4096 codebook-3 7.5 /
 // 7.9 / 10.1 / 12.4 vs 14.0 / 14.4 / 14.7 / 14.5; 22016 rows, two rounds: 28.5 / 30.2 /
 // 40.2 / 49.7 vs 24.5 / 24.9 / 40.1 / 41.4). Up to 16 rows: measured against the
-// small-batch GEMV-style
-// kernel (m <= 4) and the matrix-core GEMM on 11008x4096, 4096x11008 and 4096x4096 in all
-// thirteen formats at m = 2-16 (us, 3-bit uniform g64 at m = 2 / 8 / 16: 11008x4096 8.4 /
-// 9.0 / 9.9 against 9.2 / 15.7 / 15.8; 4096x11008 10.9 / 12.9 / 14.6 against 10.8 / 16.2 /
-// 18.1; 4096x4096 4.9 / 5.5 / 6.2 against 5.5 / 8.7 / 8.7). Rows of more than 32 chunks
-// take two or more items per lane, whose 4-bit tables of 32 or 64 codes (and, at more
-// than 4 items, any format) spill registers; Q4X, 4-bit codebooks of 128 codes and, at
-// m = 2, most formats run faster elsewhere on such rows.
+// small-batch GEMV-style kernel (m <= 4) and the matrix-core GEMM in all thirteen formats
+// (us, 3-bit uniform g64 at m = 2 / 8 / 16: 11008x4096 8.4 / 9.0 / 9.9 against 9.2 / 15.7 /
+// 15.8; 4096x4096 4.9 / 5.5 / 6.2 against 5.5 / 8.7 / 8.7). Rows of more than 32 chunks
+// (two to four items per lane, the next item's codes requested as each item is staged),
+// at m = 2 / 3 / 4 / 5 / 8 / 16: 4096x11008 uniform-3 g64 9.1 at m = 2 against 10.9 for the
+// GEMV-style kernel, 5120x13824 18.3 against 16.2 (uniform codes at m = 2 on four items
+// stay there); 4-bit codebooks of 128 codes faster at every m (4096x11008 12.4 / 12.8 /
+// 12.9 / 13.2 / 13.8 / 15.8 against 13.7 / 18.0 / 18.4 / 17.1 / 17.3 / 19.4; 5120x13824
+// 24.2 / .. / 34.1 against 24.5 / .. / 40.9), of 64 codes on two items up to m = 5 and on
+// three up to m = 3 (4096x8192 12.3 / 13.9 / 15.1 / 16.6 / 22.2 against 15.2 / 16.8 / 17.1
+// / 19.5 / 19.6); Q4X on two items up to m = 8 (4096x8192 9.8 / 10.0 / 10.1 / 11.8 / 15.2
+// against 10.1 / 12.0 / 12.4 / 17.6 / 17.5) and on three at m = 3, 4 (14.1 / 15.8 against
+// 16.2 / 16.5); 4-bit codebooks of 32 codes nowhere (their tables spill registers).
 bool gemm_skinny_applies(const qx_desc* d, int m) {
   const int C = d->k / 128, J = (C + 31) / 32;  // items per lane (8 waves of 4 chunks)
 #ifdef QX_SKINNY_FORCE
@@ -576,9 +592,13 @@ bool gemm_skinny_applies(const qx_desc* d, int m) {
     const int rf = d->n >= 8192 ? 3 : 1;
     return J == 1 && (d->n + 16 * rf - 1) / (16 * rf) <= 256 && !q4x && !(cb && d->bits == 4 && d->group <= 64);
   }
-  if (cb && d->bits == 4) return d->group >= 64 && J == 1;
-  if (q4x) return J == 1 && (m >= 3 || d->n <= 4096);
-  if (J >= 2 && m == 2) return cb && d->group >= 64;
+  if (cb && d->bits == 4) {
+    if (d->group == 128) return true;
+    if (d->group == 64) return J == 1 || (J == 2 && m <= 5) || (J == 3 && m <= 3);
+    return false;
+  }
+  if (q4x) return J == 1 ? (m >= 3 || d->n <= 4096) : J == 2 ? m <= 8 : J == 3 && m >= 3 && m <= 4;
+  if (J == 4 && m == 2) return cb;  // uniform codes at m = 2 on rows of 97-128 chunks: GEMV-style
   return true;
 }
 

@@ -41,6 +41,8 @@ CASES = [
     (16, 8200, 4096),   # the same at a full activation tile
     (7, 8193, 5120),    # C = 40: two row fragments per wave and 2 items; one row in the last block
     (6, 60, 16384),     # C = 128: 4 items, 8 waves
+    (2, 37, 11008),     # m = 2 on 3 items (uniform and codebook codes here since the one-item look-ahead)
+    (2, 20, 16384),     # m = 2 on 4 items: codebooks here, uniform codes GEMV-style
     (24, 130, 4096),    # two activation tiles, the second of 8 rows
     (33, 8200, 4096),   # three tiles (the last of one row), three row fragments per wave
     (64, 40, 384),      # four full tiles, one wave
