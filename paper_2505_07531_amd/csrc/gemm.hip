@@ -63,7 +63,9 @@ struct CodeTile {
   static constexpr int kMetaRow = KIND == QX_UNIFORM ? SC * (128 / G) * 4
                                   : KIND == QX_Q4X  ? SC * 8
                                                     : SC * (128 / G) * (2 << BITS);
-  static constexpr int kMetaStride = kMetaRow + (KIND == QX_UNIFORM ? 4 : KIND == QX_Q4X ? 8 : 16);
+  // padded by the width of a lane's table read (uniform: 4, 8 or 16 bytes for 1, 2 or 4
+  // groups per chunk), so that every read is aligned to its width
+  static constexpr int kMetaStride = kMetaRow + (KIND == QX_UNIFORM ? 4 * (128 / G) : KIND == QX_Q4X ? 8 : 16);
 };
 
 template <int BITS, int KIND, int G, int SC>
