@@ -19,7 +19,10 @@
  *     aligned and stay valid until the work queued on the stream has run.
  *   - Device calls enqueue work on `stream` (NULL = the null stream) and
  *     return without synchronizing. They allocate no memory, keep no global
- *     mutable state, and may be captured into a HIP graph.
+ *     mutable state besides a per-device cache of the compute-unit count
+ *     (filled on first use), and may be captured into a HIP graph. A launch
+ *     is checked with hipGetLastError, so a HIP error that an earlier call on
+ *     the thread left unread is reported as QX_E_HIP.
  *   - The caller owns every buffer and the stream.
  *   - Errors are negative status codes, listed below; QX_OK is 0. Argument
  *     errors are detected before anything is enqueued. An error raised by the

@@ -73,6 +73,10 @@ def load():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             _build.build()
+        try:  # torch's HIP runtime first, so that libqx binds to the one that owns torch's memory
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         P, sz = ctypes.c_void_p, ctypes.c_size_t
         D = ctypes.POINTER(QxDesc)

@@ -564,10 +564,13 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
 
 // Whether qx_gemm runs m rows on this kernel. Beyond 16 rows (several activation tiles,
 // every code decoded again per tile) only rows of at most 32 chunks with one round of
-// blocks (us at m = 24 / 32 / 48 / 64 against the matrix-core GEMM: 11008x4096 uniform-3
-// g64 15.2 / 15.7 / 21.0 / 26.5 vs 22.1 / 21.8 / 27.6 / 27.1; 4096x4096 codebook-3 7.5 /
-// 7.9 / 10.1 / 12.4 vs 14.0 / 14.4 / 14.7 / 14.5; 22016 rows, two rounds: 28.5 / 30.2 /
-// 40.2 / 49.7 vs 24.5 / 24.9 / 40.1 / 41.4). Up to 16 rows: measured against the
+// blocks (us at m = 24 / 32 / 48 / 64 against the matrix-core GEMM, weights rotated over
+// four copies: 11008x4096 uniform-3 g64 16.8 / 17.5 / 23.7 / 29.4 vs 21.6 / 21.5 / 27.5 /
+// 27.8; 12288x4096 codebook-3 15.0 / 15.8 / 20.6 / 25.5 vs 19.9 / 19.9 / 25.0 / 25.1;
+// 4096x4096 codebook-3 8.9 / 9.1 / 11.5 / 14.0 vs 14.8 / 14.9 / 15.3 / 15.5; 22016 rows,
+// two rounds: 28.5 / 30.2 / 40.2 / 49.7 vs 24.5 / 24.9 / 40.1 / 41.4; at m = 64 the tall
+// matrices' GEMM gains came from the last-level cache: with the c5 MLP's weights streamed
+// from HBM, 87.2 us per gate + up + down against 89.7 with them on the GEMM). Up to 16 rows: measured against the
 // small-batch GEMV-style kernel (m <= 4) and the matrix-core GEMM in all thirteen formats
 // (us, 3-bit uniform g64 at m = 2 / 8 / 16: 11008x4096 8.4 / 9.0 / 9.9 against 9.2 / 15.7 /
 // 15.8; 4096x4096 4.9 / 5.5 / 6.2 against 5.5 / 8.7 / 8.7). Rows of more than 32 chunks

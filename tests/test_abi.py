@@ -318,3 +318,19 @@ def test_binding_checks_tensors_against_the_descriptor():
     with pytest.raises(ValueError):
         qx.qx_gemm_a8(d, blob, 4, _FakeTensor(torch.int8, 4 * 256, shape=(4, 256)), _FakeTensor(torch.float16, 4),
                       _FakeTensor(torch.float16, 4 * 64))
+
+
+def test_load_imports_torch_before_the_library():
+    """libqx and torch must share one HIP runtime: load() imports torch (and with it the
+    runtime that owns torch's device memory) before it opens libqx, whatever the caller
+    imported first. Run in a fresh interpreter so that nothing has imported torch yet."""
+    import subprocess
+    import sys
+    code = ("import sys\n"
+            "import paper_2505_07531_amd as qx\n"
+            "assert 'torch' not in sys.modules\n"
+            "qx.load()\n"
+            "assert 'torch' in sys.modules\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]

@@ -47,6 +47,7 @@ CASES = [
     (33, 8200, 4096),   # three tiles (the last of one row), three row fragments per wave
     (64, 40, 384),      # four full tiles, one wave
     (47, 8193, 1152),   # three tiles, three fragments, one row in the last block
+    (56, 8200, 4096),   # four tiles (the last of 8 rows), three fragments per wave
     (9, 16400, 1024),   # six row fragments per wave (16384 rows or more), last block of 80 rows
     (2, 8190, 4096),    # pipelined form: two 16-row groups per compute unit, the last of 14 rows
     (16, 16390, 3840),  # pipelined, C = 30 (lane groups past the row), 4-5 groups per block, last of 6 rows
