@@ -557,10 +557,20 @@ static int launch_gemm_t(const qx_desc* d, const void* packed, int m, const void
         // 128 x 192 blocks, one per compute unit, where the last round of blocks keeps
         // most units busy (11008x4096 uniform-3 at m = 512: 110 -> 91 us, m = 1024 193
         // -> 165; 22016x4096 m = 512 183 -> 163; but 11008 rows at m = 768, two rounds
-        // with 92 blocks in the second, 166 against 167)
-        const long big = (long)((d->n + 191) / 192) * ((m + 127) / 128);
+        // with 92 blocks in the second, 166 against 167). 128 x 32 per wave in 128 x 256
+        // blocks of 8 waves (two per SIMD: about 30 % more work per compute unit in the
+        // same time) where those take fewer rounds of blocks (11008x4096 uniform-3 g64 at
+        // m = 2048: 298.7 -> 248.3 us, 12288x4096 299.6 -> 255.0, 22016x4096 at m = 1024
+        // 297.5 -> 241.0; with as many rounds, e.g. 11008 rows at m = 512, 76.8 against
+        // 79.3 for the 4-wave blocks). Not for 3-bit g32, whose 8-wave tile spills.
+        const long mb = (m + 127) / 128;
+        const long big = (long)((d->n + 191) / 192) * mb, big8 = (long)((d->n + 255) / 256) * mb;
         const long last = big % 256 == 0 ? 256 : big % 256;
-        if (QX_GEMM_CFG == 0 && m >= 384 && last >= 150)
+        constexpr bool kBig8 = !(BITS == 3 && G == 32);
+        if (kBig8 && QX_GEMM_CFG == 0 && m >= 384 && (big8 + 255) / 256 < (big + 255) / 256) {
+          if constexpr (kBig8)
+            launch_gemm_cfg<BITS, KIND, G, 8, 2, 1, QX_GEMM_BIG_S, QX_GEMM_BIG_DX, A8, 8>(d, p, m, X, sx, Y, s);
+        } else if (QX_GEMM_CFG == 0 && m >= 384 && last >= 150)
           launch_gemm_cfg<BITS, KIND, G, 8, 3, 1, QX_GEMM_BIG_S, QX_GEMM_BIG_DX, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 64) launch_gemm_cfg<BITS, KIND, G, 4, 2, 4, 1, 1, A8>(d, p, m, X, sx, Y, s);
         else if (QX_GEMM_CFG == 0 && tiles <= 128) launch_gemm_cfg<BITS, KIND, G, 4, 2, 2, 4, 2, A8>(d, p, m, X, sx, Y, s);

@@ -219,9 +219,12 @@ def test_gemm_prefill_shapes(gpu, m, name):
 
 # activation tiles mapped to XCDs with padding blocks, single-chunk rows, chunk counts
 # that leave K-split waves idle in the last round; 128 x 192 blocks (uniform formats at
-# m >= 384) with ragged weight and activation rows
+# m >= 384) with ragged weight and activation rows; 128 x 256 blocks of 8 waves where those
+# take fewer rounds (11000 rows at m = 600: last block of 248 rows, last tile of 88; 16400
+# rows at m = 384)
 GEMM_EDGES = [(40, 1024, 300), (300, 1152, 100), (17, 128, 129), (70, 640, 40), (1, 640, 17),
-              (4096, 1152, 128), (2000, 1536, 200), (9601, 1152, 390), (4800, 640, 768)]
+              (4096, 1152, 128), (2000, 1536, 200), (9601, 1152, 390), (4800, 640, 768),
+              (11000, 640, 600), (16400, 384, 384)]
 
 
 @pytest.mark.parametrize("fmt", [(3, 0, 64), (4, 0, 128), (3, 1, 32), (4, 1, 32)], ids=_fmt_id)
