@@ -202,9 +202,11 @@ constexpr int kXRow = 1024 + 16;
 // from there. Reading the fragments straight from X would touch 64 cache lines per
 // load instead of 8.
 // Loads are issued in the order the products consume them: the first tile's
-// activation rows of item 0, the first weight-row fragment of item 0, the other
-// fragments and items; the next staged rows (next item, else next tile) are loaded
-// while the current ones are multiplied.
+// activation rows of item 0, the first weight-row fragment of item 0, its other
+// fragments and those of the next QX_SKINNY_AHEAD - 1 items. When an item's rows are
+// staged, the next staged rows (next item, else next tile) are requested, then the codes
+// of the item QX_SKINNY_AHEAD ahead: a wave's loads return in order, so rows requested
+// behind all of its codes would wait for every one of them.
 // LDS: W * min(m, 16) rows of kXRow bytes, reused after each activation tile for the
 // W * RF tiles of 16 x 16 fp32 that are added in wave order.
 template <int BITS, int KIND, int G, int RF, int J, int LB, int MT>
