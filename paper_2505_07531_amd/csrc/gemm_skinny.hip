@@ -368,7 +368,8 @@ __device__ __forceinline__ void mul_group(const Item<BITS, KIND, G> (&it)[RF], c
 template <int BITS, int KIND, int G, int RF, int NB>
 __global__ __launch_bounds__(512) void gemm_skinny_loop_kernel(const char* __restrict__ packed,
                                                                const uint16_t* __restrict__ X,
-                                                               uint16_t* __restrict__ Y, int n, int k, int m) {
+                                                               uint16_t* __restrict__ Y, int n, int k, int m,
+                                                               int slot_off, int slot_stride) {
   constexpr int W = 8;
   extern __shared__ __align__(16) char lds[];
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
@@ -418,15 +419,17 @@ __global__ __launch_bounds__(512) void gemm_skinny_loop_kernel(const char* __res
 #pragma unroll
     for (int P = 0; P < 16; ++P) a[P] = *reinterpret_cast<const h8_t*>(src + 16 * P);
   }
-  __syncthreads();  // every wave holds its fragments (and the Q4X tables are staged)
-
-  // wave tiles of group s at red[(s * W + wave) * RF * 256 ..], over the staged rows;
-  // the waves run through their groups without waiting for each other
-  float* red = reinterpret_cast<float*>(lds);
+  // Wave tiles of group s at lds + slot_off + wave * slot_stride + s * RF KB: past the
+  // staged rows, where no wave waits for another before its products (one barrier
+  // precedes the sums); or, where LDS is short (m near 16), over the wave's own staged
+  // rows, which it has read (one wave's LDS instructions execute in order), after a
+  // barrier that keeps the waves in step as they start (measured faster there).
+  if (KIND == QX_Q4X || slot_off == 0) __syncthreads();  // (the Q4X tables are staged)
+  float* const myslots = reinterpret_cast<float*>(lds + slot_off + (size_t)wave * slot_stride);
   auto product = [&](const Item<BITS, KIND, G>(&cur)[RF], int st) {
     f4_t acc[RF];
     mul_group<BITS, KIND, G, RF>(cur, a, q4lut, valid, kc, acc);
-    float* rd = red + (st * W + wave) * RF * 256;
+    float* rd = myslots + st * RF * 256;
 #pragma unroll
     for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(rd + f * 256 + 4 * lane) = acc[f];
   };
@@ -465,10 +468,10 @@ __global__ __launch_bounds__(512) void gemm_skinny_loop_kernel(const char* __res
     const int cc = oo % (16 * RF), r = oo / (16 * RF);
     const int f = cc >> 4;
     const int idx = f * 256 + 4 * (16 * (r >> 2) + (cc & 15)) + (r & 3);
-    const float* rd = red + st * W * RF * 256;
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < W; ++w) sum += rd[w * RF * 256 + idx];
+    for (int w = 0; w < W; ++w)
+      sum += reinterpret_cast<const float*>(lds + slot_off + (size_t)w * slot_stride)[st * RF * 256 + idx];
     const int n0 = ((int)blockIdx.x + st * (int)gridDim.x) * 16 * RF;
     if (r < rows && n0 + cc < n) Y[(size_t)r * n + n0 + cc] = (uint16_t)float_to_half_bits(sum);
   }
@@ -491,15 +494,33 @@ inline int compute_units() {
   return v;
 }
 
+// LDS of the pipelined form for m rows and `tiles` group tiles per wave: each wave's
+// tiles past the 8 waves' staged rows where that fits, else over the wave's own staged
+// rows; 0 if neither fits.
+inline size_t loop_lds(int m, int tiles, int* slot_off, int* slot_stride) {
+  const int rows_bytes = std::min(m, 16) * kXRow, slots_bytes = tiles * 1024;
+  if (8 * (rows_bytes + slots_bytes) <= 160 * 1024) {
+    *slot_off = 8 * rows_bytes; *slot_stride = slots_bytes;
+    return (size_t)8 * (rows_bytes + slots_bytes);
+  }
+  if (slots_bytes <= rows_bytes) {
+    *slot_off = 0; *slot_stride = rows_bytes;
+    return (size_t)8 * rows_bytes;
+  }
+  return 0;
+}
+
 template <int BITS, int KIND, int G, int RF, int NB>
 int launch_loop(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16_t* Y, hipStream_t s) {
   const int groups = (d->n + 16 * RF - 1) / (16 * RF), blocks = compute_units();
   const int steps = (groups + blocks - 1) / blocks;
   if (groups / blocks < NB || m > 16 || d->k / 128 > 32) return QX_E_UNSUPPORTED;  // every block holds NB groups
-  const size_t lds = std::max((size_t)8 * std::min(m, 16) * kXRow, (size_t)steps * 8 * RF * 256 * sizeof(float));
+  int slot_off, slot_stride;
+  const size_t lds = loop_lds(m, steps * RF, &slot_off, &slot_stride);
+  if (lds == 0) return QX_E_UNSUPPORTED;
   if (lds > 160 * 1024) return QX_E_UNSUPPORTED;
   hipLaunchKernelGGL((gemm_skinny_loop_kernel<BITS, KIND, G, RF, NB>), dim3((unsigned)blocks), dim3(512), lds, s, p, X, Y,
-                     d->n, d->k, m);
+                     d->n, d->k, m, slot_off, slot_stride);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 
@@ -546,7 +567,8 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
     // one-shot form, or four groups or more (measured; see the kernel's comment)
     const int groups = (d->n + 15) / 16, cus = compute_units();
     const int steps = (groups + cus - 1) / cus;
-    if (groups / cus >= 2 && steps <= 20 && (steps < rf || steps >= 4))
+    int so, ss;
+    if (groups / cus >= 2 && (steps < rf || steps >= 4) && loop_lds(m, steps, &so, &ss) > 0)
       return launch_loop<BITS, KIND, G, 1, 2>(d, p, m, X, Y, s);
   }
 #define QX_SKINNY_J(JJ)                                                                                   \
