@@ -37,7 +37,9 @@
 // groups or more, rows of at most 32 chunks at m <= 16 take that form (22016x4096
 // uniform-4 g128 at m = 2 / 16: 16.0 / 17.6 us -> 13.8 / 15.2; 16400x4096 uniform-3 g64
 // 13.6 / 15.3 -> 10.8 / 12.2; 8192x4096 7.9 / 9.3 -> 7.0 / 8.5; 11008 and 12288 rows,
-// 48 rows per compute unit in both forms: the one-shot form measured equal or faster).
+// 48 rows per compute unit in both forms: the one-shot form measured equal or faster,
+// except for Q4X at m >= 3: 11008x4096 13.8 / 14.3 / 15.1 -> 12.6 / 12.5 / 13.3 at m = 4 /
+// 8 / 16, 12288x4096 14.0 / 14.6 / 15.4 -> 12.5 / 12.7 / 13.6).
 // qx_gemm routes m rows here where it measured faster (gemm_skinny_applies).
 #include <atomic>
 #include <utility>
@@ -481,6 +483,7 @@ __global__ __launch_bounds__(512) void gemm_skinny_loop_kernel(const char* __res
 #define QX_SKINNY_LOOP 1  // 0: the one-shot form only
 #endif
 
+
 // Compute units of the current device (cached per device).
 inline int compute_units() {
   static std::atomic<int> cus[64];
@@ -568,7 +571,8 @@ int launch_t(const qx_desc* d, const void* packed, int m, const uint16_t* X, uin
     const int groups = (d->n + 15) / 16, cus = compute_units();
     const int steps = (groups + cus - 1) / cus;
     int so, ss;
-    if (groups / cus >= 2 && (steps < rf || steps >= 4) && loop_lds(m, steps, &so, &ss) > 0)
+    const bool q4x3 = KIND == QX_Q4X && m >= 3;  // Q4X at m >= 3 whenever every unit holds two groups
+    if (groups / cus >= 2 && (q4x3 || steps < rf || steps >= 4) && loop_lds(m, steps, &so, &ss) > 0)
       return launch_loop<BITS, KIND, G, 1, 2>(d, p, m, X, Y, s);
   }
 #define QX_SKINNY_J(JJ)                                                                                   \
