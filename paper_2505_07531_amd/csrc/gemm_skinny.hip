@@ -209,12 +209,15 @@ constexpr int kXRow = 1024 + 16;
 // staged, the next staged rows (next item, else next tile) are requested, then the codes
 // of the item QX_SKINNY_AHEAD ahead: a wave's loads return in order, so rows requested
 // behind all of its codes would wait for every one of them.
-// LDS: W * min(m, 16) rows of kXRow bytes, reused after each activation tile for the
-// W * RF tiles of 16 x 16 fp32 that are added in wave order.
+// LDS: W * min(m, 16) rows of kXRow bytes and the W * RF tiles of 16 x 16 fp32 that are
+// added in wave order, past the rows where LDS allows (then one barrier per activation
+// tile orders the tiles' writes after the previous sums, and a wave stages and multiplies
+// the next tile meanwhile), else over them after each tile.
 template <int BITS, int KIND, int G, int RF, int J, int LB, int MT>
 __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict__ packed,
                                                          const uint16_t* __restrict__ X,
-                                                         uint16_t* __restrict__ Y, int n, int k, int m) {
+                                                         uint16_t* __restrict__ Y, int n, int k, int m,
+                                                         int red_off) {
   extern __shared__ __align__(16) char lds[];
   __shared__ __align__(16) uint32_t q4lut[KIND == QX_Q4X ? 32 : 1];
   const int C = k >> 7, G_row = k / G, W = blockDim.x >> 6;
@@ -225,7 +228,8 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
   const DecodeConsts kc = decode_consts();
   const int mtiles = (m + 15) >> 4, rows0 = min(m, 16);
   char* xs = lds + (size_t)wave * rows0 * kXRow;  // this wave's activation rows (one 16-row tile)
-  float* red = reinterpret_cast<float*>(lds);      // W * RF tiles of 16 x 16, over the staged rows
+  // W * RF tiles of 16 x 16: past the staged rows (red_off > 0) where LDS allows, else over them
+  float* red = reinterpret_cast<float*>(lds + red_off);
 
   Item<BITS, KIND, G> it[J][RF];
   auto load_frag = [&](int j, int f) {  // rows and chunks clamped in bounds
@@ -307,9 +311,10 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
       }
     }
 
-    // wave tiles -> LDS over the staged rows (every wave is past its reads of them):
-    // red[(w * RF + f) * 256 + 4 * lane + r] holds D[4 g + r][li]
-    __syncthreads();
+    // wave tiles -> LDS: red[(w * RF + f) * 256 + 4 * lane + r] holds D[4 g + r][li]. Over
+    // the staged rows every wave must be past its reads of them; past them only past the
+    // previous tile's sums (so a wave stages and multiplies the next tile meanwhile)
+    if (red_off == 0 || mt > 0) __syncthreads();
 #pragma unroll
     for (int f = 0; f < RF; ++f) *reinterpret_cast<f4_t*>(red + (wave * RF + f) * 256 + 4 * lane) = acc[f];
     __syncthreads();
@@ -323,7 +328,7 @@ __global__ __launch_bounds__(LB) void gemm_skinny_kernel(const char* __restrict_
       for (int w = 0; w < W; ++w) s += red[w * RF * 256 + idx];
       if (r < rows && n0 + c < n) Y[(size_t)(16 * mt + r) * n + n0 + c] = (uint16_t)float_to_half_bits(s);
     }
-    if (mt + 1 < mtiles) __syncthreads();  // the sums are read before the next tile is staged
+    if (red_off == 0 && mt + 1 < mtiles) __syncthreads();  // the sums are read before the next tile is staged
   }
 }
 
@@ -532,14 +537,17 @@ int launch_cfg(const qx_desc* d, const char* p, int m, const uint16_t* X, uint16
   const int C = d->k / 128;
   const int W = (C + 4 * J - 1) / (4 * J);
   if (W > LB / 64 || m > 64) return QX_E_UNSUPPORTED;
-  const size_t lds = std::max((size_t)W * std::min(m, 16) * kXRow, (size_t)W * RF * 256 * sizeof(float));
+  const size_t rows_bytes = (size_t)W * std::min(m, 16) * kXRow, red_bytes = (size_t)W * RF * 256 * sizeof(float);
+  const bool sep = rows_bytes + red_bytes <= 160 * 1024;  // reduction tiles past the staged rows
+  const size_t lds = sep ? rows_bytes + red_bytes : std::max(rows_bytes, red_bytes);
+  const int red_off = sep ? (int)rows_bytes : 0;
   const unsigned blocks = (unsigned)((d->n + 16 * RF - 1) / (16 * RF));
   if (m <= 16)
     hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB, 1>), dim3(blocks), dim3(64 * W), lds, s, p, X,
-                       Y, d->n, d->k, m);
+                       Y, d->n, d->k, m, red_off);
   else
     hipLaunchKernelGGL((gemm_skinny_kernel<BITS, KIND, G, RF, J, LB, 4>), dim3(blocks), dim3(64 * W), lds, s, p, X,
-                       Y, d->n, d->k, m);
+                       Y, d->n, d->k, m, red_off);
   return hipGetLastError() == hipSuccess ? QX_OK : QX_E_HIP;
 }
 
